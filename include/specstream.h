@@ -1,0 +1,178 @@
+/*
+ * specstream.h -- C ABI of the chunk-streamed speculative-verification
+ * attention library (libspecstream.so, gfx950 / MI355X).
+ *
+ * What it computes (paper Sec. 4.2, "KV Streaming for Multi-Query
+ * Verification"): in one verification round every request b of a Cohort has
+ * n_b candidate queries (the k_b draft tokens plus one, at positions C_b + i)
+ * that attend to
+ *   - the committed history [0, C_b), delivered as chunks of tokens that are
+ *     each read once for all n_b * Hq queries of the request (Sec. 4.2,
+ *     "chunked verification shared across queries"), and
+ *   - the GPU-resident Speculative Frontier (Eq. 8): candidate keys j with
+ *     j <= i (causal mask by absolute position, Sec. 4.2).
+ * The result equals full attention (Eq. 12, Eq. 17): per query and head an
+ * online-softmax state (m, l, a) starts at (-inf, 0, 0) (Sec. 4.2), each chunk
+ * contributes its local state (Eq. 13) through the rescaled merge (Eq. 14),
+ * and O = a / l at the end.
+ *
+ * Conventions shared by every call
+ *   - bf16 = IEEE bfloat16 bit patterns (uint16); all device arrays are
+ *     row-major and 16-byte aligned.
+ *   - Query rows are packed in request order: row (b, i) = off_b + i with
+ *     off_b = sum_{b'<b} n_b'.  Q and O are [sum n_b, Hq, d]; candidate K/V
+ *     are [sum n_b, Hkv, d].
+ *   - A history chunk is token-major [sum_b len_b, Hkv, d] with request b's
+ *     len_b tokens contiguous and requests in order, so a Cohort's chunk is
+ *     one contiguous buffer (K and V are two such buffers).
+ *   - GQA: query head h reads KV head floor(h / G), G = Hq / Hkv.
+ *   - Q and K arrive with any positional encoding applied; softmax_scale
+ *     multiplies the dot product (1/sqrt(d) in the paper, Sec. 4.2).
+ *   - Ownership: the caller owns every buffer, stream and event and keeps
+ *     them alive until the enqueued work has finished.  The library never
+ *     allocates device memory; its only state is the host handle.
+ *   - Asynchrony: calls validate, enqueue on the given stream and return.
+ *     A non-OK status means nothing was enqueued by that call (except
+ *     SS_ERR_HIP, reported when a launch itself fails).  Device faults
+ *     surface at the caller's synchronisation.
+ *   - All calls of one round go to one stream (or are ordered by events);
+ *     calls of one round that overlap on different streams race.
+ *   - Threading: one host thread per handle at a time.  ss_last_error() is
+ *     thread-local.
+ */
+#ifndef SPECSTREAM_H
+#define SPECSTREAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ss_round ss_round;       /* opaque host handle of one round */
+typedef struct ss_pipeline ss_pipeline; /* opaque two-slot upload pipeline */
+typedef int32_t ss_status;
+
+enum {
+  SS_OK = 0,
+  SS_ERR_INVALID_ARGUMENT = -1, /* null/misaligned pointer, bad size or count */
+  SS_ERR_UNSUPPORTED = -2,      /* valid but not built: head_dim != 128, rows per KV head > 32 */
+  SS_ERR_BAD_STATE = -3,        /* call out of order for this round */
+  SS_ERR_NOT_PINNED = -4,       /* upload source is not pinned (page-locked) host memory */
+  SS_ERR_WORKSPACE = -5,        /* workspace null, misaligned or too small */
+  SS_ERR_HIP = -6               /* a HIP runtime call failed (detail in ss_last_error) */
+};
+
+/* Largest candidate count per request (k_b + 1).  The paper's widths are
+ * q in {2, 4, 6, 8} (Sec. 5.1). */
+#define SS_MAX_CANDIDATES 8
+/* Rows that share one KV head, n_b * Hq / Hkv, must not exceed this. */
+#define SS_MAX_ROWS_PER_KV_HEAD 32
+
+typedef struct {
+  int32_t num_requests;     /* B >= 1: one Cohort (Sec. 4.2, Cohort batching)  */
+  int32_t num_q_heads;      /* Hq >= 1, Hq % Hkv == 0                          */
+  int32_t num_kv_heads;     /* Hkv >= 1                                        */
+  int32_t head_dim;         /* d; only 128 is built (else SS_ERR_UNSUPPORTED)  */
+  float softmax_scale;      /* sigma > 0, finite; 1/sqrt(d) in the paper       */
+  const int32_t *num_cand;  /* host [B]: n_b = k_b + 1, 1 <= n_b <= 8, copied  */
+  int32_t max_chunk_tokens; /* >= 1: bound on sum_b len_b of one history call  */
+  int32_t split_tokens;     /* tokens per workgroup piece; 0 = automatic;
+                               else a multiple of 32                           */
+  int32_t mfma_min_rows;    /* rows per KV head (n_b * G) from which the bf16
+                               MFMA path is used; fewer use the fp32 VALU path.
+                               0 = default (8); 1 = always MFMA; 33 = never    */
+} ss_round_desc;
+
+/* Bytes of device workspace a round with this descriptor needs (fp32
+ * online-softmax states of every query row, per split slot).  0 if the
+ * descriptor is invalid (see ss_last_error). */
+size_t ss_round_workspace_bytes(const ss_round_desc *desc);
+
+/* Start a round (paper Sec. 4.2: state (m, l, a) = (-inf, 0, 0) per query and
+ * head).  q: device bf16 [sum n_b, Hq, d], read by the later calls, so it
+ * must stay unchanged until ss_round_finalize has run.  workspace: device,
+ * 256-byte aligned, >= ss_round_workspace_bytes(desc); owned by the round
+ * until finalize has run.  Enqueues one small kernel on `stream`.
+ * On success *out receives a new handle (free with ss_round_destroy). */
+ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q,
+                        void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Copy one history chunk (or any byte range) from pinned host memory to the
+ * device on a side stream (paper Sec. 4.2, "Pipelined KV transfers": chunks
+ * move host->device while the previous chunk is being attended).
+ * If wait_before is non-null, copy_stream first waits for it (the staging
+ * slot's "free" event); if signal_after is non-null it is recorded on
+ * copy_stream after the copy (the slot's "ready" event).  src must be
+ * page-locked host memory (hipHostMalloc / pinned tensors), else
+ * SS_ERR_NOT_PINNED; dst must be device memory.  bytes > 0. */
+ss_status ss_upload_chunk(void *dst_device, const void *src_pinned_host, size_t bytes,
+                          hipStream_t copy_stream, hipEvent_t wait_before, hipEvent_t signal_after);
+
+/* Attend one history chunk for every request of the round (paper Sec. 4.2:
+ * S_j = Q K_j^T / sqrt(d) for the whole query group, Eq. 13 local state,
+ * Eq. 14 merge into the running state).  k, v: device bf16 [sum_b len_b, Hkv, d]
+ * (layout above).  len: host [B], len_b >= 0 (0 = request has no tokens in
+ * this chunk), sum <= max_chunk_tokens.  History tokens are visible to every
+ * candidate query.  Chunks may come in any order and any number (>= 0),
+ * before or after ss_attend_local_candidates.  If wait_before is non-null the
+ * stream waits for it first (chunk ready); if signal_after is non-null it is
+ * recorded after the last kernel reading k and v (chunk buffer free). */
+ss_status ss_attend_history_chunk(ss_round *r, const void *k, const void *v, const int32_t *len,
+                                  hipEvent_t wait_before, hipEvent_t signal_after, hipStream_t stream);
+
+/* Attend the Speculative Frontier (paper Sec. 4.2, GPU-resident pass): query
+ * i of request b sees candidate keys j <= i of the same request.  k_cand,
+ * v_cand: device bf16 [sum n_b, Hkv, d].  Exactly once per round. */
+ss_status ss_attend_local_candidates(ss_round *r, const void *k_cand, const void *v_cand,
+                                     hipStream_t stream);
+
+/* Finish the round: merge the split states (Eq. 14) and write O = a / l
+ * (paper Sec. 4.2, Eq. 17).  out: device fp32 [sum n_b, Hq, d].  lse: null or
+ * device fp32 [sum n_b, Hq], natural-log sum of exp of the scaled scores
+ * (m + ln l).  Requires ss_attend_local_candidates to have been called.
+ * After finalize the handle accepts no more calls except destroy. */
+ss_status ss_round_finalize(ss_round *r, float *out, float *lse, hipStream_t stream);
+
+/* Free the host handle (never device memory).  Null is ignored.  Call it
+ * after enqueueing finalize; enqueued work does not use the handle. */
+void ss_round_destroy(ss_round *r);
+
+/* Two-slot host->device pipeline (paper Sec. 4.2: two GPU staging buffers,
+ * separate transfer and compute streams; buffer A is attended while B
+ * receives the next chunk, and a buffer is refilled only after the whole
+ * query group has consumed it).  staging0/1: device buffers of slot_bytes
+ * each, owned by the caller.  copy_stream: the transfer stream.  The
+ * pipeline owns four events (ready/free per slot), created here. */
+ss_status ss_pipeline_create(ss_pipeline **out, void *staging0, void *staging1, size_t slot_bytes,
+                             hipStream_t copy_stream);
+
+/* Upload one history chunk into the next staging slot and attend it:
+ *   copy_stream: wait free[s]; copy host_kv -> slot s; record ready[s]
+ *   stream:      wait ready[s]; ss_attend_history_chunk; record free[s]
+ * host_kv: pinned host bf16 [2][sum_b len_b][Hkv][d] (the chunk's K then its
+ * V, contiguous), len as in ss_attend_history_chunk.  The chunk may belong
+ * to any round (e.g. the next layer), so transfers run ahead across layer
+ * boundaries. */
+ss_status ss_pipeline_attend_chunk(ss_pipeline *p, ss_round *r, const void *host_kv,
+                                   const int32_t *len, hipStream_t stream);
+
+/* Destroy the pipeline's events (after its work has completed). */
+void ss_pipeline_destroy(ss_pipeline *p);
+
+/* Event helpers so callers need no HIP binding of their own.  Events are
+ * created with timing disabled. */
+ss_status ss_event_create(hipEvent_t *e);
+void ss_event_destroy(hipEvent_t e);
+
+/* Static description of a status code. */
+const char *ss_status_string(ss_status s);
+/* Detail of the last failure on this thread ("" if none). */
+const char *ss_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPECSTREAM_H */

@@ -1,0 +1,444 @@
+// Host side of libspecstream: argument validation, the round state machine,
+// the work planner that splits each history chunk into workgroup pieces, the
+// upload call and the two-slot transfer pipeline (paper Sec. 4.2).
+#include "specstream.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "ss_kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ss_status fail(ss_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+ss_status hip_fail(hipError_t e, const char *what) {
+  return fail(SS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Workgroups one history call aims for (2 resident per CU on 256 CUs).
+constexpr long kTargetWorkgroups = 512;
+constexpr int kMinPiece = 256;
+constexpr int kDefaultMfmaMinRows = ss::kMaxValuRows + 1;
+
+ss_status validate_desc(const ss_round_desc *d) {
+  if (d == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "desc is null");
+  if (d->num_requests < 1) return fail(SS_ERR_INVALID_ARGUMENT, "num_requests must be >= 1 (got %d)", d->num_requests);
+  if (d->num_q_heads < 1 || d->num_kv_heads < 1)
+    return fail(SS_ERR_INVALID_ARGUMENT, "head counts must be >= 1 (Hq=%d, Hkv=%d)", d->num_q_heads, d->num_kv_heads);
+  if (d->num_q_heads % d->num_kv_heads != 0)
+    return fail(SS_ERR_INVALID_ARGUMENT, "num_q_heads (%d) must be a multiple of num_kv_heads (%d)", d->num_q_heads,
+                d->num_kv_heads);
+  if (d->head_dim != ss::kHeadDim)
+    return fail(SS_ERR_UNSUPPORTED, "head_dim %d is not built (only %d)", d->head_dim, ss::kHeadDim);
+  if (!(d->softmax_scale > 0.f) || !std::isfinite(d->softmax_scale))
+    return fail(SS_ERR_INVALID_ARGUMENT, "softmax_scale must be finite and > 0");
+  if (d->num_cand == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "num_cand is null");
+  if (d->max_chunk_tokens < 1) return fail(SS_ERR_INVALID_ARGUMENT, "max_chunk_tokens must be >= 1");
+  if (d->split_tokens < 0 || d->split_tokens % ss::kTile != 0)
+    return fail(SS_ERR_INVALID_ARGUMENT, "split_tokens must be 0 or a positive multiple of %d", ss::kTile);
+  if (d->mfma_min_rows < 0 || d->mfma_min_rows > ss::kMaxValuRows + 1)
+    return fail(SS_ERR_INVALID_ARGUMENT, "mfma_min_rows must be in [0, %d]", ss::kMaxValuRows + 1);
+  const int G = d->num_q_heads / d->num_kv_heads;
+  long rows = 0;
+  for (int b = 0; b < d->num_requests; ++b) {
+    const int n = d->num_cand[b];
+    if (n < 1 || n > SS_MAX_CANDIDATES)
+      return fail(SS_ERR_INVALID_ARGUMENT, "num_cand[%d] = %d outside [1, %d]", b, n, SS_MAX_CANDIDATES);
+    if (n * G > SS_MAX_ROWS_PER_KV_HEAD)
+      return fail(SS_ERR_UNSUPPORTED, "request %d: n_b * Hq/Hkv = %d rows per KV head exceeds %d", b, n * G,
+                  SS_MAX_ROWS_PER_KV_HEAD);
+    rows += (long)n * d->num_q_heads;
+  }
+  if (rows * (long)ss::kNumSlots * ss::kHeadDim > (1L << 40))
+    return fail(SS_ERR_INVALID_ARGUMENT, "round too large");
+  return SS_OK;
+}
+
+size_t workspace_bytes_rows(long R) {
+  const size_t a = align_up((size_t)ss::kNumSlots * R * ss::kHeadDim * sizeof(float), 256);
+  const size_t m = align_up((size_t)ss::kNumSlots * R * sizeof(float), 256);
+  return a + 2 * m;
+}
+
+}  // namespace
+
+struct ss_round {
+  int32_t B, Hq, Hkv, G;
+  float scale;
+  int32_t max_chunk_tokens, split_tokens, mfma_min_rows;
+  std::vector<int32_t> n_cand, row_off;
+  const uint16_t *q;
+  ss::State st;
+  bool cand_done = false;
+  bool finalized = false;
+};
+
+struct ss_pipeline {
+  char *slot[2];
+  size_t slot_bytes;
+  hipStream_t copy;
+  hipEvent_t ready[2];
+  hipEvent_t freed[2];
+  bool used[2];
+  int next;
+};
+
+namespace {
+
+ss_status check_round(const ss_round *r) {
+  if (r == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "round handle is null");
+  if (r->finalized) return fail(SS_ERR_BAD_STATE, "round already finalized");
+  return SS_OK;
+}
+
+// Validate a history call's arguments; total tokens in *total.
+ss_status check_history_args(const ss_round *r, const int32_t *len, long *total) {
+  ss_status s = check_round(r);
+  if (s != SS_OK) return s;
+  if (len == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "len is null");
+  long t = 0;
+  for (int b = 0; b < r->B; ++b) {
+    if (len[b] < 0) return fail(SS_ERR_INVALID_ARGUMENT, "len[%d] = %d < 0", b, len[b]);
+    t += len[b];
+  }
+  if (t > r->max_chunk_tokens)
+    return fail(SS_ERR_INVALID_ARGUMENT, "chunk has %ld tokens > max_chunk_tokens %d", t, r->max_chunk_tokens);
+  *total = t;
+  return SS_OK;
+}
+
+struct Plan {
+  std::vector<ss::Item> valu, rb1, rb2;
+};
+
+// Split every request's tokens of this chunk into pieces of `piece` tokens;
+// piece p of a request folds into state slot p.
+void plan_chunk(const ss_round *r, const int32_t *len, long total, Plan *plan) {
+  int max_len = 0;
+  for (int b = 0; b < r->B; ++b) max_len = std::max(max_len, len[b]);
+  long piece;
+  if (r->split_tokens > 0) {
+    piece = r->split_tokens;
+  } else {
+    const long work = total * r->Hkv;
+    piece = (work + kTargetWorkgroups - 1) / kTargetWorkgroups;
+    piece = std::max<long>(kMinPiece, align_up(piece, ss::kTile));
+  }
+  const long min_piece = align_up((max_len + ss::kNumSlots - 1) / ss::kNumSlots, ss::kTile);
+  piece = std::max(piece, min_piece);
+  const int min_rows = r->mfma_min_rows > 0 ? r->mfma_min_rows : kDefaultMfmaMinRows;
+  long off = 0;
+  for (int b = 0; b < r->B; ++b) {
+    const int n = len[b];
+    const int M = r->n_cand[b] * r->G;
+    std::vector<ss::Item> *dst = (M < min_rows && M <= ss::kMaxValuRows) ? &plan->valu
+                                 : (M <= 16)                             ? &plan->rb1
+                                                                         : &plan->rb2;
+    for (long p0 = 0, slot = 0; p0 < n; p0 += piece, ++slot) {
+      ss::Item it;
+      it.tok_begin = (int32_t)(off + p0);
+      it.tok_count = (int32_t)std::min<long>(piece, n - p0);
+      it.q_row0 = r->row_off[b];
+      it.n_cand = (int16_t)r->n_cand[b];
+      it.slot = (int16_t)slot;
+      dst->push_back(it);
+    }
+    off += n;
+  }
+  // longest pieces first (a partial piece never delays the tail of the grid)
+  auto by_len = [](const ss::Item &a, const ss::Item &b) { return a.tok_count > b.tok_count; };
+  std::stable_sort(plan->valu.begin(), plan->valu.end(), by_len);
+  std::stable_sort(plan->rb1.begin(), plan->rb1.end(), by_len);
+  std::stable_sort(plan->rb2.begin(), plan->rb2.end(), by_len);
+}
+
+ss::ChunkParams *base_params(const ss_round *r, const void *k, const void *v) {
+  static thread_local ss::ChunkParams p;
+  p.k = static_cast<const uint16_t *>(k);
+  p.v = static_cast<const uint16_t *>(v);
+  p.q = r->q;
+  p.st = r->st;
+  p.Hq = r->Hq;
+  p.Hkv = r->Hkv;
+  p.G = r->G;
+  p.scale_log2 = r->scale * 1.4426950408889634f;
+  p.num_items = 0;
+  return &p;
+}
+
+// Launch `items` in batches of kMaxItems with `launch(params)`.
+template <typename F>
+hipError_t launch_items(ss::ChunkParams *p, const std::vector<ss::Item> &items, F launch) {
+  for (size_t i0 = 0; i0 < items.size(); i0 += ss::kMaxItems) {
+    const size_t n = std::min<size_t>(ss::kMaxItems, items.size() - i0);
+    std::memcpy(p->items, items.data() + i0, n * sizeof(ss::Item));
+    p->num_items = (int32_t)n;
+    const hipError_t e = launch(*p);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+ss_status enqueue_history(ss_round *r, const void *k, const void *v, const int32_t *len, long total,
+                          hipStream_t stream) {
+  if (total == 0) return SS_OK;
+  Plan plan;
+  plan_chunk(r, len, total, &plan);
+  ss::ChunkParams *p = base_params(r, k, v);
+  hipError_t e = launch_items(p, plan.rb2, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 2, stream); });
+  if (e == hipSuccess)
+    e = launch_items(p, plan.rb1, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 1, stream); });
+  if (e == hipSuccess)
+    e = launch_items(p, plan.valu,
+                     [&](const ss::ChunkParams &q) { return ss::launch_chunk_valu(q, ss::kMaxValuRows, stream); });
+  if (e != hipSuccess) return hip_fail(e, "history chunk kernel launch");
+  return SS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ss_round_workspace_bytes(const ss_round_desc *desc) {
+  if (validate_desc(desc) != SS_OK) return 0;
+  long R = 0;
+  for (int b = 0; b < desc->num_requests; ++b) R += (long)desc->num_cand[b] * desc->num_q_heads;
+  return workspace_bytes_rows(R);
+}
+
+ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+  if (out == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "out is null");
+  *out = nullptr;
+  ss_status s = validate_desc(desc);
+  if (s != SS_OK) return s;
+  if (q == nullptr || !aligned(q, 16)) return fail(SS_ERR_INVALID_ARGUMENT, "q must be non-null and 16-byte aligned");
+  long R = 0;
+  for (int b = 0; b < desc->num_requests; ++b) R += (long)desc->num_cand[b] * desc->num_q_heads;
+  const size_t need = workspace_bytes_rows(R);
+  if (workspace == nullptr || !aligned(workspace, 256))
+    return fail(SS_ERR_WORKSPACE, "workspace must be non-null and 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(SS_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+
+  ss_round *r = new (std::nothrow) ss_round();
+  if (r == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "out of host memory");
+  r->B = desc->num_requests;
+  r->Hq = desc->num_q_heads;
+  r->Hkv = desc->num_kv_heads;
+  r->G = r->Hq / r->Hkv;
+  r->scale = desc->softmax_scale;
+  r->max_chunk_tokens = desc->max_chunk_tokens;
+  r->split_tokens = desc->split_tokens;
+  r->mfma_min_rows = desc->mfma_min_rows;
+  r->n_cand.assign(desc->num_cand, desc->num_cand + desc->num_requests);
+  r->row_off.resize(r->B);
+  int32_t acc = 0;
+  for (int b = 0; b < r->B; ++b) {
+    r->row_off[b] = acc;
+    acc += r->n_cand[b];
+  }
+  r->q = static_cast<const uint16_t *>(q);
+  char *ws = static_cast<char *>(workspace);
+  const size_t a_bytes = align_up((size_t)ss::kNumSlots * R * ss::kHeadDim * sizeof(float), 256);
+  const size_t m_bytes = align_up((size_t)ss::kNumSlots * R * sizeof(float), 256);
+  r->st.a = reinterpret_cast<float *>(ws);
+  r->st.m = reinterpret_cast<float *>(ws + a_bytes);
+  r->st.l = reinterpret_cast<float *>(ws + a_bytes + m_bytes);
+  r->st.R = (int32_t)R;
+  const hipError_t e = ss::launch_init_state(r->st, stream);
+  if (e != hipSuccess) {
+    delete r;
+    return hip_fail(e, "state init launch");
+  }
+  *out = r;
+  return SS_OK;
+}
+
+ss_status ss_upload_chunk(void *dst_device, const void *src_pinned_host, size_t bytes, hipStream_t copy_stream,
+                          hipEvent_t wait_before, hipEvent_t signal_after) {
+  if (dst_device == nullptr || src_pinned_host == nullptr)
+    return fail(SS_ERR_INVALID_ARGUMENT, "upload pointers must be non-null");
+  if (bytes == 0) return fail(SS_ERR_INVALID_ARGUMENT, "upload of 0 bytes");
+  hipPointerAttribute_t attr;
+  std::memset(&attr, 0, sizeof attr);
+  hipError_t e = hipPointerGetAttributes(&attr, src_pinned_host);
+  if (e != hipSuccess || attr.type != hipMemoryTypeHost) {
+    (void)hipGetLastError();
+    return fail(SS_ERR_NOT_PINNED, "upload source %p is not pinned host memory", src_pinned_host);
+  }
+  std::memset(&attr, 0, sizeof attr);
+  e = hipPointerGetAttributes(&attr, dst_device);
+  if (e != hipSuccess || attr.type != hipMemoryTypeDevice) {
+    (void)hipGetLastError();
+    return fail(SS_ERR_INVALID_ARGUMENT, "upload destination %p is not device memory", dst_device);
+  }
+  if (wait_before != nullptr && (e = hipStreamWaitEvent(copy_stream, wait_before, 0)) != hipSuccess)
+    return hip_fail(e, "hipStreamWaitEvent (upload)");
+  if ((e = hipMemcpyAsync(dst_device, src_pinned_host, bytes, hipMemcpyHostToDevice, copy_stream)) != hipSuccess)
+    return hip_fail(e, "hipMemcpyAsync (upload)");
+  if (signal_after != nullptr && (e = hipEventRecord(signal_after, copy_stream)) != hipSuccess)
+    return hip_fail(e, "hipEventRecord (upload)");
+  return SS_OK;
+}
+
+ss_status ss_attend_history_chunk(ss_round *r, const void *k, const void *v, const int32_t *len,
+                                  hipEvent_t wait_before, hipEvent_t signal_after, hipStream_t stream) {
+  long total = 0;
+  ss_status s = check_history_args(r, len, &total);
+  if (s != SS_OK) return s;
+  if (total > 0 && (k == nullptr || v == nullptr || !aligned(k, 16) || !aligned(v, 16)))
+    return fail(SS_ERR_INVALID_ARGUMENT, "k and v must be non-null and 16-byte aligned");
+  hipError_t e;
+  if (wait_before != nullptr && (e = hipStreamWaitEvent(stream, wait_before, 0)) != hipSuccess)
+    return hip_fail(e, "hipStreamWaitEvent (history)");
+  s = enqueue_history(r, k, v, len, total, stream);
+  if (s != SS_OK) return s;
+  if (signal_after != nullptr && (e = hipEventRecord(signal_after, stream)) != hipSuccess)
+    return hip_fail(e, "hipEventRecord (history)");
+  return SS_OK;
+}
+
+ss_status ss_attend_local_candidates(ss_round *r, const void *k_cand, const void *v_cand, hipStream_t stream) {
+  ss_status s = check_round(r);
+  if (s != SS_OK) return s;
+  if (r->cand_done) return fail(SS_ERR_BAD_STATE, "local candidates already attended for this round");
+  if (k_cand == nullptr || v_cand == nullptr || !aligned(k_cand, 16) || !aligned(v_cand, 16))
+    return fail(SS_ERR_INVALID_ARGUMENT, "k_cand and v_cand must be non-null and 16-byte aligned");
+  std::vector<ss::Item> items(r->B);
+  for (int b = 0; b < r->B; ++b) {
+    items[b].tok_begin = 0;
+    items[b].tok_count = 0;
+    items[b].q_row0 = r->row_off[b];
+    items[b].n_cand = (int16_t)r->n_cand[b];
+    items[b].slot = 0;
+  }
+  ss::ChunkParams *p = base_params(r, k_cand, v_cand);
+  const hipError_t e = launch_items(p, items, [&](const ss::ChunkParams &q) { return ss::launch_candidates(q, stream); });
+  if (e != hipSuccess) return hip_fail(e, "candidate kernel launch");
+  r->cand_done = true;
+  return SS_OK;
+}
+
+ss_status ss_round_finalize(ss_round *r, float *out, float *lse, hipStream_t stream) {
+  ss_status s = check_round(r);
+  if (s != SS_OK) return s;
+  if (!r->cand_done) return fail(SS_ERR_BAD_STATE, "finalize before ss_attend_local_candidates");
+  if (out == nullptr || !aligned(out, 16)) return fail(SS_ERR_INVALID_ARGUMENT, "out must be non-null and 16-byte aligned");
+  if (lse != nullptr && !aligned(lse, 4)) return fail(SS_ERR_INVALID_ARGUMENT, "lse must be 4-byte aligned");
+  const hipError_t e = ss::launch_finalize(r->st, out, lse, stream);
+  if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
+  r->finalized = true;
+  return SS_OK;
+}
+
+void ss_round_destroy(ss_round *r) { delete r; }
+
+ss_status ss_pipeline_create(ss_pipeline **out, void *staging0, void *staging1, size_t slot_bytes,
+                             hipStream_t copy_stream) {
+  if (out == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "out is null");
+  *out = nullptr;
+  if (staging0 == nullptr || staging1 == nullptr || !aligned(staging0, 256) || !aligned(staging1, 256))
+    return fail(SS_ERR_INVALID_ARGUMENT, "staging slots must be non-null and 256-byte aligned");
+  if (slot_bytes == 0) return fail(SS_ERR_INVALID_ARGUMENT, "slot_bytes must be > 0");
+  ss_pipeline *p = new (std::nothrow) ss_pipeline();
+  if (p == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "out of host memory");
+  p->slot[0] = static_cast<char *>(staging0);
+  p->slot[1] = static_cast<char *>(staging1);
+  p->slot_bytes = slot_bytes;
+  p->copy = copy_stream;
+  p->used[0] = p->used[1] = false;
+  p->next = 0;
+  for (int i = 0; i < 2; ++i) {
+    hipError_t e = hipEventCreateWithFlags(&p->ready[i], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&p->freed[i], hipEventDisableTiming);
+    if (e != hipSuccess) {
+      for (int j = 0; j < i; ++j) {
+        (void)hipEventDestroy(p->ready[j]);
+        (void)hipEventDestroy(p->freed[j]);
+      }
+      delete p;
+      return hip_fail(e, "pipeline event creation");
+    }
+  }
+  *out = p;
+  return SS_OK;
+}
+
+ss_status ss_pipeline_attend_chunk(ss_pipeline *p, ss_round *r, const void *host_kv, const int32_t *len,
+                                   hipStream_t stream) {
+  if (p == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "pipeline is null");
+  long total = 0;
+  ss_status s = check_history_args(r, len, &total);
+  if (s != SS_OK) return s;
+  if (total == 0) return SS_OK;
+  if (host_kv == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "host_kv is null");
+  const size_t half = (size_t)total * r->Hkv * ss::kHeadDim * 2;
+  if (2 * half > p->slot_bytes)
+    return fail(SS_ERR_INVALID_ARGUMENT, "chunk needs %zu bytes > slot_bytes %zu", 2 * half, p->slot_bytes);
+  const int sl = p->next;
+  s = ss_upload_chunk(p->slot[sl], host_kv, 2 * half, p->copy, p->used[sl] ? p->freed[sl] : nullptr, p->ready[sl]);
+  if (s != SS_OK) return s;
+  s = ss_attend_history_chunk(r, p->slot[sl], p->slot[sl] + half, len, p->ready[sl], p->freed[sl], stream);
+  if (s != SS_OK) return s;
+  p->used[sl] = true;
+  p->next = sl ^ 1;
+  return SS_OK;
+}
+
+void ss_pipeline_destroy(ss_pipeline *p) {
+  if (p == nullptr) return;
+  for (int i = 0; i < 2; ++i) {
+    (void)hipEventDestroy(p->ready[i]);
+    (void)hipEventDestroy(p->freed[i]);
+  }
+  delete p;
+}
+
+ss_status ss_event_create(hipEvent_t *e) {
+  if (e == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "event pointer is null");
+  const hipError_t h = hipEventCreateWithFlags(e, hipEventDisableTiming);
+  if (h != hipSuccess) return hip_fail(h, "hipEventCreateWithFlags");
+  return SS_OK;
+}
+
+void ss_event_destroy(hipEvent_t e) {
+  if (e != nullptr) (void)hipEventDestroy(e);
+}
+
+const char *ss_status_string(ss_status s) {
+  switch (s) {
+    case SS_OK: return "SS_OK";
+    case SS_ERR_INVALID_ARGUMENT: return "SS_ERR_INVALID_ARGUMENT";
+    case SS_ERR_UNSUPPORTED: return "SS_ERR_UNSUPPORTED";
+    case SS_ERR_BAD_STATE: return "SS_ERR_BAD_STATE";
+    case SS_ERR_NOT_PINNED: return "SS_ERR_NOT_PINNED";
+    case SS_ERR_WORKSPACE: return "SS_ERR_WORKSPACE";
+    case SS_ERR_HIP: return "SS_ERR_HIP";
+    default: return "SS_ERR_UNKNOWN";
+  }
+}
+
+const char *ss_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

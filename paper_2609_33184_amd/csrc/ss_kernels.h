@@ -1,0 +1,61 @@
+// Internal interface between the host library (ss_host.cpp) and the gfx950
+// kernels (ss_kernels.hip).  Not part of the public ABI.
+#pragma once
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace ss {
+
+constexpr int kHeadDim = 128;       // d
+constexpr int kNumSlots = 16;       // split slots of the running state per row
+constexpr int kMaxItems = 200;      // work items per launch (kernel-argument list)
+constexpr int kTile = 32;           // history tokens per wave iteration
+constexpr int kWaves = 4;           // waves per workgroup of the chunk kernels
+constexpr int kMaxCand = 8;         // candidates per request (k_b + 1)
+constexpr int kMaxValuRows = 4;     // rows per KV head the VALU chunk kernel handles
+constexpr int kMaxRows = 32;        // rows per KV head the MFMA chunk kernel handles
+
+// One workgroup's share of a history chunk for one request (x all KV heads
+// through blockIdx.y): tokens [tok_begin, tok_begin + tok_count) of the packed
+// chunk, folded into split slot `slot` of the request's query rows.
+struct Item {
+  int32_t tok_begin;
+  int32_t tok_count;
+  int32_t q_row0;   // off_b: first packed candidate row of the request
+  int16_t n_cand;   // n_b
+  int16_t slot;
+};
+static_assert(sizeof(Item) == 16, "Item layout");
+
+// Running state in the workspace, per slot s and query row R_idx = (off_b+i)*Hq+h:
+//   m[s*R + R_idx]   running max of sigma*log2(e)*q.k (log2 domain), -inf = empty
+//   l[s*R + R_idx]   running sum of 2^(x - m)
+//   a[(s*R + R_idx)*d + c]  running weighted value sum (same scale as l)
+struct State {
+  float *m;
+  float *l;
+  float *a;
+  int32_t R;        // rows = sum n_b * Hq
+};
+
+struct ChunkParams {
+  const uint16_t *k;    // bf16 [sum len, Hkv, d]
+  const uint16_t *v;
+  const uint16_t *q;    // bf16 [sum n_b, Hq, d]
+  State st;
+  int32_t Hq, Hkv, G;
+  float scale_log2;     // softmax_scale * log2(e)
+  int32_t num_items;
+  Item items[kMaxItems];
+};
+
+// Launch wrappers; return hipGetLastError() of the launch.
+hipError_t launch_init_state(const State &st, hipStream_t s);
+hipError_t launch_chunk_mfma(const ChunkParams &p, int row_blocks, hipStream_t s);
+hipError_t launch_chunk_valu(const ChunkParams &p, int max_rows, hipStream_t s);
+// Candidates: p.k / p.v are the candidate K / V [sum n_b, Hkv, d]; one item per
+// request (q_row0, n_cand; token fields unused), merged into slot 0.
+hipError_t launch_candidates(const ChunkParams &p, hipStream_t s);
+hipError_t launch_finalize(const State &st, float *out, float *lse, hipStream_t s);
+
+}  // namespace ss

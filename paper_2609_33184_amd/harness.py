@@ -1,0 +1,136 @@
+"""Device buffers and round drivers over the C ABI (used by tests, bench, smoke).
+
+Torch provides device memory, pinned host memory and streams only; every step
+of the round runs in libspecstream's kernels through the binding.
+"""
+from __future__ import annotations
+
+from typing import List, Optional, Sequence, Tuple
+
+import torch
+
+from . import specstream as ss
+from .workloads import Workload
+
+BF16_BYTES = 2
+
+
+class RoundBuffers:
+    """Queries, candidate K/V, workspace and outputs of one layer's round."""
+
+    def __init__(self, w: Workload, layer: int = 0, device="cuda", split_tokens: int = 0,
+                 mfma_min_rows: int = 0, max_chunk_tokens: Optional[int] = None):
+        self.w = w
+        self.layer = layer
+        self.device = device
+        self.q = w.q_all(layer, device)
+        self.kc = w.k_cand_all(layer, device)
+        self.vc = w.v_cand_all(layer, device)
+        mct = max_chunk_tokens or max(1, max(sum(w.chunk_lens(j)) for j in range(max(1, w.num_chunks))))
+        self.desc = ss.make_desc(w.num_cand, w.num_q_heads, w.num_kv_heads, w.head_dim, w.softmax_scale,
+                                 mct, split_tokens, mfma_min_rows)
+        self.ws_bytes = ss.ss_round_workspace_bytes(self.desc)
+        if self.ws_bytes == 0:
+            raise ss.SpecStreamError(ss.SS_ERR_INVALID_ARGUMENT, "ss_round_workspace_bytes", ss.ss_last_error())
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        rows = w.total_rows
+        self.out = torch.empty(rows, w.num_q_heads, w.head_dim, dtype=torch.float32, device=device)
+        self.lse = torch.empty(rows, w.num_q_heads, dtype=torch.float32, device=device)
+
+    def set_layer(self, layer: int) -> None:
+        """New per-layer queries (candidates and history are shared by layers)."""
+        self.layer = layer
+        self.q.copy_(self.w.q_all(layer, self.device))
+
+
+def hbm_history(w: Workload, layer: int = 0, device="cuda") -> List[Tuple[torch.Tensor, torch.Tensor]]:
+    """Every history chunk resident in device memory: [(k_j, v_j)]."""
+    return [w.chunk_kv(j, layer, device) for j in range(w.num_chunks)]
+
+
+def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor]], stream: int,
+              order: Optional[Sequence[int]] = None, cand_position: Optional[int] = None,
+              lens: Optional[Sequence[Sequence[int]]] = None) -> None:
+    """Enqueue one whole round (init, history chunks, candidates, finalize)
+    on `stream`; results land in b.out / b.lse."""
+    w = b.w
+    order = list(range(len(chunks))) if order is None else list(order)
+    pos = len(order) if cand_position is None else cand_position
+    r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream)
+    try:
+        for idx, j in enumerate(order):
+            if idx == pos:
+                ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
+            k, v = chunks[j]
+            ln = w.chunk_lens(j) if lens is None else lens[j]
+            ss.ss_attend_history_chunk(r, k.data_ptr() if k.numel() else 0, v.data_ptr() if v.numel() else 0,
+                                       ln, None, None, stream)
+        if pos >= len(order):
+            ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
+        ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream)
+    finally:
+        ss.ss_round_destroy(r)
+
+
+class HostHistory:
+    """One layer's history in pinned host memory, chunk j as [2][sum len_bj][Hkv][d]
+    (its K then its V), for streaming through the two-slot pipeline."""
+
+    def __init__(self, w: Workload, layer: int = 0, gen_device="cuda"):
+        self.w = w
+        tb = w.num_kv_heads * w.head_dim * BF16_BYTES
+        self.sizes = [2 * sum(w.chunk_lens(j)) * tb for j in range(w.num_chunks)]
+        self.offsets = []
+        acc = 0
+        for s in self.sizes:
+            self.offsets.append(acc)
+            acc += s
+        self.total_bytes = acc
+        self.buf = torch.empty(max(1, acc), dtype=torch.uint8, pin_memory=True)
+        for j in range(w.num_chunks):
+            if self.sizes[j] == 0:
+                continue
+            k, v = w.chunk_kv(j, layer, gen_device)
+            half = self.sizes[j] // 2
+            o = self.offsets[j]
+            self.buf[o:o + half].copy_(k.view(-1).view(torch.uint8).cpu())
+            self.buf[o + half:o + 2 * half].copy_(v.view(-1).view(torch.uint8).cpu())
+            del k, v
+
+    def chunk_ptr(self, j: int) -> int:
+        return self.buf.data_ptr() + self.offsets[j]
+
+    def max_chunk_bytes(self) -> int:
+        return max(self.sizes) if self.sizes else 0
+
+
+class Pipeline:
+    """The library's two-slot pipeline with its staging buffers and copy stream."""
+
+    def __init__(self, slot_bytes: int, device="cuda"):
+        self.slot_bytes = max(256, slot_bytes)
+        self.staging = [torch.empty(self.slot_bytes, dtype=torch.uint8, device=device) for _ in range(2)]
+        self.copy_stream = torch.cuda.Stream(device=device)          # default priority
+        self.handle = ss.ss_pipeline_create(self.staging[0].data_ptr(), self.staging[1].data_ptr(),
+                                            self.slot_bytes, self.copy_stream.cuda_stream)
+
+    def close(self) -> None:
+        if self.handle:
+            torch.cuda.synchronize()
+            ss.ss_pipeline_destroy(self.handle)
+            self.handle = None
+
+
+def run_round_streamed(b: RoundBuffers, host: HostHistory, pipe: Pipeline, stream: int,
+                       order: Optional[Sequence[int]] = None) -> None:
+    """Enqueue one round whose history streams from pinned host memory."""
+    w = b.w
+    order = list(range(w.num_chunks)) if order is None else list(order)
+    r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream)
+    try:
+        for j in order:
+            ss.ss_pipeline_attend_chunk(pipe.handle, r, host.chunk_ptr(j), w.chunk_lens(j), stream)
+        ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
+        ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream)
+    finally:
+        ss.ss_round_destroy(r)

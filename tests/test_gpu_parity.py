@@ -1,0 +1,121 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Small workloads are compared element by element on every output row; the
+full-size workloads (the five configurations, in the launch configuration
+the benchmark times) on sampled (request, KV head) groups the oracle
+recomputes from regenerated slices.  Bar: max-abs <= 2e-3 and rel-L2 <= 1e-3.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_33184_amd import harness as H
+from paper_2609_33184_amd import specstream as ss
+from paper_2609_33184_amd import workloads as W
+from parity import assert_parity, check_sampled, oracle_full
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def stream():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    ss.load()
+    s = torch.cuda.Stream()
+    yield s
+    torch.cuda.synchronize()
+
+
+def _run(w, stream, **kw):
+    b = H.RoundBuffers(w, split_tokens=kw.pop("split_tokens", 0), mfma_min_rows=kw.pop("mfma_min_rows", 0))
+    chunks = H.hbm_history(w)
+    torch.cuda.synchronize()
+    H.run_round(b, chunks, stream.cuda_stream, **kw)
+    stream.synchronize()
+    return b
+
+
+def _full_check(w, b, what):
+    ref_o, ref_l = oracle_full(w)
+    assert_parity(b.out.double().cpu().numpy(), ref_o, what)
+    assert_parity(b.lse.double().cpu().numpy(), ref_l, what + " lse", max_abs=1e-3, rel_l2=1e-4)
+
+
+def test_config1_tiny_full(stream):
+    w = W.workload(1)
+    print("config 1 tiny, in-HBM", flush=True)
+    b = _run(w, stream)
+    _full_check(w, b, "config1")
+
+
+def test_config1_tiny_forced_paths(stream):
+    w = W.workload(1)
+    for split in (32, 96, 1024):
+        print(f"config 1, split_tokens={split}", flush=True)
+        b = _run(w, stream, split_tokens=split, mfma_min_rows=1)
+        _full_check(w, b, f"config1 split={split}")
+
+
+def test_config2_full(stream):
+    w = W.workload(2)
+    print("config 2, in-HBM", flush=True)
+    b = _run(w, stream)
+    _full_check(w, b, "config2")
+
+
+def test_config3_sampled_full_size(stream):
+    w = W.workload(3)
+    print("config 3 (16 x 32768), in-HBM, bench launch configuration", flush=True)
+    b = _run(w, stream)
+    check_sampled(w, b.out, b.lse, [(0, 0), (7, 3), (15, 7)], what="config3")
+
+
+def test_config4_sampled_full_size(stream):
+    w = W.workload(4)
+    print("config 4 (ragged 64), in-HBM", flush=True)
+    b = _run(w, stream)
+    lens = np.array(w.hist_len)
+    cands = np.array(w.num_cand)
+    pick = {int(lens.argmax()), int(lens.argmin()), int(np.where(cands == 1)[0][0]),
+            int(np.where(cands == 8)[0][0]), int(np.where(cands == 4)[0][0])}
+    pairs = [(bb, (3 * bb) % w.num_kv_heads) for bb in sorted(pick)]
+    check_sampled(w, b.out, b.lse, pairs, what="config4")
+
+
+def test_config5_one_layer_full_size(stream):
+    w = W.workload(5)
+    print("config 5 (32 x 131072, outliers), one layer in-HBM", flush=True)
+    b = _run(w, stream)
+    check_sampled(w, b.out, b.lse, [(0, 1), (31, 6)], what="config5 layer0")
+
+
+def test_small_edge_cases(stream):
+    cases = [
+        ([0], [1], 8, 2),                # empty history, decode
+        ([0, 0], [3, 8], 8, 2),          # empty history, candidates only
+        ([1], [1], 8, 2),                # a single history token
+        ([33, 31, 1000], [8, 1, 4], 8, 2),
+        ([4096, 0, 77], [2, 5, 1], 32, 8),
+        ([300], [3], 8, 8),              # G = 1
+        ([257, 513], [4, 2], 64, 8),     # G = 8: 32 rows per KV head
+    ]
+    for k, (lens, cands, hq, hkv) in enumerate(cases):
+        w = W.custom(lens, cands, num_q_heads=hq, num_kv_heads=hkv, chunk_tokens=256, seed_base=40 + k)
+        for mfma_min_rows in (0, 1):
+            print(f"edge case {k}: lens={lens} cands={cands} Hq={hq} Hkv={hkv} mfma_min_rows={mfma_min_rows}",
+                  flush=True)
+            b = _run(w, stream, mfma_min_rows=mfma_min_rows)
+            _full_check(w, b, f"edge{k}/{mfma_min_rows}")
+
+
+def test_valu_and_mfma_paths_agree_with_oracle(stream):
+    w = W.custom([3000, 1777], [1, 1], num_q_heads=32, num_kv_heads=8, chunk_tokens=1024, seed_base=7)
+    outs = []
+    for mmr in (5, 1):          # 5: n_b*G = 4 rows -> VALU; 1: always MFMA
+        print(f"decode rows, mfma_min_rows={mmr}", flush=True)
+        b = _run(w, stream, mfma_min_rows=mmr)
+        _full_check(w, b, f"decode mfma_min_rows={mmr}")
+        outs.append(b.out.clone())
+    assert (outs[0] - outs[1]).abs().max().item() <= 1e-4
