@@ -81,8 +81,10 @@ __device__ __forceinline__ int global_row(const ChunkParams &p, const Item &it, 
 template <int ROWS>
 __device__ __forceinline__ void fold_into_slot(const ChunkParams &p, const Item &it, int g, int M,
                                                const float *aw, const float *mw, const float *lw) {
-  constexpr int SEGS = 256 / ROWS;
+  // SEGS threads per row, SEGLEN (a multiple of 4) values each
+  constexpr int SEGS = (256 / ROWS) < 32 ? (256 / ROWS) : 32;
   constexpr int SEGLEN = kHeadDim / SEGS;
+  static_assert(SEGLEN % 4 == 0 && SEGS * ROWS <= 256, "fold layout");
   const int r = threadIdx.x / SEGS;
   const int seg = threadIdx.x % SEGS;
   if (r >= M) return;
