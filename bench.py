@@ -180,6 +180,8 @@ def main() -> int:
     ap.add_argument("--cpu-sample-requests", type=int, default=6)
     ap.add_argument("--per-launch-only", action="store_true",
                     help="only time the history-chunk launches (for profiler runs)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run a plain 1 GiB device-to-device copy (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); "
@@ -194,6 +196,15 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
+    if args.copy_probe:
+        n = 1 << 30
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy probe: 3 copies of {n} bytes")
+        return 0
     ss.load()
     w = W.workload(args.config)
     log(f"bench: config {args.config} ({w.name}): generating inputs on the GPU")

@@ -23,6 +23,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace ss {
 namespace {
 
@@ -31,7 +33,6 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr float kNegInf = -__builtin_huge_valf();
-constexpr int kVtPitch = 40;   // bf16 per transposed V row (32 tokens + pad): 80 B
 constexpr int kAwPitch = 132;  // floats per row of a wave's partial accumulator
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -154,20 +155,42 @@ __device__ __forceinline__ void fold_into_slot(const ChunkParams &p, const Item 
 //   S^T[t][row] = K Q^T      v_mfma_f32_16x16x32_bf16, A = K (16 tokens x 32 d
 //                            from registers), B = Q^T (held in registers)
 //   online softmax per row   (row = lane % 16; the four lane groups share it)
-//   O^T[d][row] += V^T P^T   A = V^T from a transposed LDS tile, B = P^T
-//                            straight from the S accumulators (hi and lo)
+//   O^T[d][row] += V^T P^T   A = V^T read from a row-major LDS tile with the
+//                            LDS transpose read, B = P^T straight from the S
+//                            accumulators (hi and lo parts)
 // Lane l: lr = l % 16, lq = l / 16.  In the S tile lane (lr, lq) holds
-// tokens 4*lq + r (r = 0..3) of row lr; in O it holds d = 16*db + 4*lq + r.
-// The reduction index of both MFMAs is permuted so that every operand is one
-// 16-byte read: QK^T lane group lq, k-step s covers d-chunk 4*s + lq of 8
-// values; PV lane group lq covers tokens {4lq..4lq+3, 16+4lq..16+4lq+3}.
+// tokens 16u + 4*lq + r (u = 0,1; r = 0..3) of row lr; in O it holds
+// d = 16*db + 4*lq + r.  The reduction index of both MFMAs is permuted so
+// every operand is contiguous: for QK^T lane group lq, k-step s covers the
+// d-chunk 4*s + lq (8 values); for PV lane group lq covers tokens
+// {4lq..4lq+3, 16+4lq..16+4lq+3}, exactly the S values the lane holds.
+//
+// ds_read_b64_tr_b16: within each 16-lane group, result lane i, element e is
+// element (i % 4) of what source lane 4e + i/4 addressed.  Source lane j of
+// group lq addresses row 4lq + j/4 (+16 for the second half), columns
+// 16db + 4(j%4) .. +3, so result lane i receives V[4lq + e][16db + i].
+//
+// Each wave keeps the next tile's K and V in flight in registers: K(i+1) is
+// issued as soon as S(i) has consumed K(i), V(i+1) as soon as V(i) is staged
+// in LDS, so at the top of an iteration only K is waited for.  The last tile
+// is peeled so the in-loop prefetch is unconditional (a conditional load
+// would make the compiler wait for every outstanding load).
 // ---------------------------------------------------------------------------
+constexpr int kVPitch = 144;   // bf16 per LDS V row (128 + 16): rows 288 B apart
+
 template <int RB>
 struct MfmaLds {
-  static constexpr int kVtBytes = kWaves * kHeadDim * kVtPitch * 2;
+  static constexpr int kVBytes = kWaves * kTile * kVPitch * 2;
   static constexpr int kMergeBytes = kWaves * RB * 16 * (kAwPitch + 2) * 4;
-  static constexpr int kBytes = kVtBytes > kMergeBytes ? kVtBytes : kMergeBytes;
+  static constexpr int kBytes = kVBytes > kMergeBytes ? kVBytes : kMergeBytes;
 };
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ s16x4_t lds_read_tr16(const uint16_t *p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4_t *)(reinterpret_cast<uintptr_t>(p)));
+}
 
 template <int RB>
 __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
@@ -206,10 +229,11 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
     for (int db = 0; db < 8; ++db) acc[rb][db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  const size_t tok_stride = (size_t)p.Hkv * kHeadDim;   // elements between tokens
+  // 32-bit element offsets inside the item (the host keeps an item < 2^30 elements)
+  const uint32_t tok_stride = (uint32_t)p.Hkv * kHeadDim;
   const uint16_t *kbase = p.k + ((size_t)it.tok_begin * p.Hkv + g) * kHeadDim;
   const uint16_t *vbase = p.v + ((size_t)it.tok_begin * p.Hkv + g) * kHeadDim;
-  uint16_t *vt = reinterpret_cast<uint16_t *>(smem) + w * (kHeadDim * kVtPitch);
+  uint16_t *vs = reinterpret_cast<uint16_t *>(smem) + w * (kTile * kVPitch);
   const int ntiles = (count + kTile - 1) / kTile;
   const float sl2 = p.scale_log2;
 
@@ -218,8 +242,8 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   auto load_k = [&](int tb) {
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const int t = min(tb + 16 * u + lr, count - 1);
-      const u32x4_t *src = reinterpret_cast<const u32x4_t *>(kbase + (size_t)t * tok_stride);
+      const uint32_t t = (uint32_t)min(tb + 16 * u + lr, count - 1);
+      const u32x4_t *src = reinterpret_cast<const u32x4_t *>(kbase + t * tok_stride);
 #pragma unroll
       for (int s = 0; s < 4; ++s) kr[u][s] = src[4 * s + lq];
     }
@@ -227,32 +251,15 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   auto load_v = [&](int tb) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int t = min(tb + 4 * i + lq, count - 1);
-      vr[i] = reinterpret_cast<const u32x4_t *>(vbase + (size_t)t * tok_stride)[lr];
+      const uint32_t t = (uint32_t)min(tb + 4 * i + lq, count - 1);
+      vr[i] = reinterpret_cast<const u32x4_t *>(vbase + t * tok_stride)[lr];
     }
   };
+  // V operand read addresses (row 4lq + lr/4, column 4*(lr%4)), first half
+  const uint16_t *vrd = vs + (4 * lq + (lr >> 2)) * kVPitch + 4 * (lr & 3);
 
-  int tile = w;
-  if (tile < ntiles) {
-    load_k(tile * kTile);
-    load_v(tile * kTile);
-  }
-  for (; tile < ntiles; tile += kWaves) {
-    const int tb = tile * kTile;
-    const bool more = tile + kWaves < ntiles;
-    // V tile -> LDS, transposed: vt[d][pos], pos = 8*q' + 4*u + r for token 16u + 4q' + r
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int pos = 8 * (i & 3) + 4 * (i >> 2) + lq;
-      uint16_t *dst = vt + (8 * lr) * kVtPitch + pos;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        dst[(2 * e) * kVtPitch] = (uint16_t)(vr[i][e] & 0xffffu);
-        dst[(2 * e + 1) * kVtPitch] = (uint16_t)(vr[i][e] >> 16);
-      }
-    }
-    if (more) load_v(tb + kWaves * kTile);
-
+  auto tile = [&](int tb, auto prefetch) {
+    constexpr bool kPrefetch = decltype(prefetch)::value;
     // S^T = K Q^T
     f32x4_t sacc[2][RB];
 #pragma unroll
@@ -265,7 +272,8 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
           c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[u][s]), qop[rb][s], c, 0, 0, 0);
         sacc[u][rb] = c;
       }
-    if (more) load_k(tb + kWaves * kTile);
+    if constexpr (kPrefetch) load_k(tb + kWaves * kTile);
+    __builtin_amdgcn_sched_barrier(0);   // keep the prefetch here, ahead of the softmax
 
     // online softmax (Eq. 13 local terms merged per Eq. 14 into the wave's state)
     bf16x8_t phi[RB], plo[RB];
@@ -302,16 +310,34 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
       for (int db = 0; db < 8; ++db) acc[rb][db] *= alpha;
     }
 
+    // V tile -> LDS, row-major (token 4i + lq, 16-byte chunk lr); then prefetch
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      *reinterpret_cast<u32x4_t *>(vs + (4 * i + lq) * kVPitch + 8 * lr) = vr[i];
+    if constexpr (kPrefetch) load_v(tb + kWaves * kTile);
+    __builtin_amdgcn_sched_barrier(0);   // keep the prefetch here, ahead of PV
+
     // O^T += V^T P^T  (hi and lo parts of P)
 #pragma unroll
     for (int db = 0; db < 8; ++db) {
-      const bf16x8_t vop = *reinterpret_cast<const bf16x8_t *>(vt + (16 * db + lr) * kVtPitch + 8 * lq);
+      const s16x4_t v0 = lds_read_tr16(vrd + 16 * db);
+      const s16x4_t v1 = lds_read_tr16(vrd + 16 * kVPitch + 16 * db);
+      const bf16x8_t vop = __builtin_bit_cast(
+          bf16x8_t, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         acc[rb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, phi[rb], acc[rb][db], 0, 0, 0);
         acc[rb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, plo[rb], acc[rb][db], 0, 0, 0);
       }
     }
+  };
+
+  int t0 = w;
+  if (t0 < ntiles) {
+    load_k(t0 * kTile);   // same issue order as the loop body: K, then V
+    load_v(t0 * kTile);
+    for (; t0 + kWaves < ntiles; t0 += kWaves) tile(t0 * kTile, std::integral_constant<bool, true>{});
+    tile(t0 * kTile, std::integral_constant<bool, false>{});
   }
 
   // wave partials -> LDS
@@ -334,7 +360,6 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   __syncthreads();
   fold_into_slot<RB * 16>(p, it, g, M, aw, mw, lw);
 }
-
 // ---------------------------------------------------------------------------
 // VALU chunk kernel for sparse query groups (few rows per KV head): fp32 dot
 // products on the vector ALUs, exact fp32 softmax weights.  Lane l: d-chunk
