@@ -113,8 +113,12 @@ def cpu_baseline(w, chunks, sample_requests):
             lens = w.chunk_lens(j)
             off = sum(lens[:b])
             if lens[b]:
-                ks.append(k[off:off + lens[b]].cpu())
-                vs.append(v[off:off + lens[b]].cpu())
+                if k.shape[0] == w.num_kv_heads and k.shape[1] == sum(lens):   # head-major chunk
+                    ks.append(k[:, off:off + lens[b]].transpose(0, 1).cpu())
+                    vs.append(v[:, off:off + lens[b]].transpose(0, 1).cpu())
+                else:
+                    ks.append(k[off:off + lens[b]].cpu())
+                    vs.append(v[off:off + lens[b]].cpu())
         host.append((bf16_bits(w.q(b)), bf16_bits(torch.cat(ks)), bf16_bits(torch.cat(vs)),
                      bf16_bits(w.k_cand(b)), bf16_bits(w.v_cand(b))))
     t0 = time.perf_counter()
@@ -134,7 +138,7 @@ def cpu_baseline(w, chunks, sample_requests):
 
 def streamed_round(torch, H, w, b, stream, rounds: int):
     log("streamed: filling pinned host history")
-    host = H.HostHistory(w)
+    host = H.HostHistory(w, kv_layout=b.kv_layout)
     pipe = H.Pipeline(host.max_chunk_bytes())
     try:
         for _ in range(2):
@@ -175,6 +179,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--split-tokens", type=int, default=0)
+    ap.add_argument("--kv-layout", choices=["token", "head"], default="head",
+                    help="history chunk layout: token-major [tok][Hkv][d] or head-major [Hkv][tok][d]")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-streamed", action="store_true")
     ap.add_argument("--cpu-sample-requests", type=int, default=6)
@@ -208,8 +214,9 @@ def main() -> int:
     ss.load()
     w = W.workload(args.config)
     log(f"bench: config {args.config} ({w.name}): generating inputs on the GPU")
-    b = H.RoundBuffers(w, split_tokens=args.split_tokens)
-    chunks = H.hbm_history(w)
+    layout = ss.SS_KV_HEAD_MAJOR if args.kv_layout == "head" else ss.SS_KV_TOKEN_MAJOR
+    b = H.RoundBuffers(w, split_tokens=args.split_tokens, kv_layout=layout)
+    chunks = H.hbm_history(w, kv_layout=layout)
     stream = torch.cuda.Stream()
     torch.cuda.synchronize()
 
@@ -258,7 +265,7 @@ def main() -> int:
             "workload": f"config {args.config}: {w.B} requests x {w.hist_len[0] if len(set(w.hist_len)) == 1 else 'ragged'} "
                         f"history tokens, {w.num_q_heads}q/{w.num_kv_heads}kv heads, d={w.head_dim}, "
                         f"{w.num_chunks} chunks of {w.chunk_tokens}, {w.num_cand[0] if len(set(w.num_cand)) == 1 else 'ragged'} "
-                        f"candidate queries, history resident in HBM",
+                        f"candidate queries, history resident in HBM ({args.kv_layout}-major chunks)",
             "round_latency_ms": round(step_s * 1e3, 4),
             "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
             "kv_bytes_per_round": kv_bytes,

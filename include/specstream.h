@@ -82,9 +82,19 @@ typedef struct {
   int32_t split_tokens;     /* tokens per workgroup piece; 0 = automatic;
                                else a multiple of 32                           */
   int32_t mfma_min_rows;    /* rows per KV head (n_b * G) from which the bf16
-                               MFMA path is used; fewer use the fp32 VALU path.
-                               0 = default (8); 1 = always MFMA; 33 = never    */
+                               MFMA path is used; fewer (at most 4) use the
+                               fp32 VALU path.  0 = default (5: groups of <= 4
+                               rows on VALU); 1 = always MFMA; range 0..5      */
+  int32_t kv_layout;        /* layout of history chunks: SS_KV_TOKEN_MAJOR
+                               [sum_b len_b][Hkv][d] or SS_KV_HEAD_MAJOR
+                               [Hkv][sum_b len_b][d]                           */
 } ss_round_desc;
+
+/* History chunk layouts (ss_round_desc.kv_layout).  In both, request b's
+ * len_b tokens follow request b-1's; head-major keeps each KV head's tokens
+ * contiguous (one contiguous stream per workgroup). */
+#define SS_KV_TOKEN_MAJOR 0
+#define SS_KV_HEAD_MAJOR 1
 
 /* Bytes of device workspace a round with this descriptor needs (fp32
  * online-softmax states of every query row, per split slot).  0 if the
@@ -93,9 +103,11 @@ size_t ss_round_workspace_bytes(const ss_round_desc *desc);
 
 /* Start a round (paper Sec. 4.2: state (m, l, a) = (-inf, 0, 0) per query and
  * head).  q: device bf16 [sum n_b, Hq, d], read by the later calls, so it
- * must stay unchanged until ss_round_finalize has run.  workspace: device,
- * 256-byte aligned, >= ss_round_workspace_bytes(desc); owned by the round
- * until finalize has run.  Enqueues one small kernel on `stream`.
+ * must stay unchanged until ss_round_finalize's work has completed.
+ * workspace: device, 256-byte aligned, >= ss_round_workspace_bytes(desc);
+ * owned by the round until finalize's work has completed.  The empty state
+ * is tracked on the host (a split slot is written before it is ever read),
+ * so this call currently enqueues nothing on `stream`.
  * On success *out receives a new handle (free with ss_round_destroy). */
 ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q,
                         void *workspace, size_t workspace_bytes, hipStream_t stream);
@@ -113,8 +125,9 @@ ss_status ss_upload_chunk(void *dst_device, const void *src_pinned_host, size_t 
 
 /* Attend one history chunk for every request of the round (paper Sec. 4.2:
  * S_j = Q K_j^T / sqrt(d) for the whole query group, Eq. 13 local state,
- * Eq. 14 merge into the running state).  k, v: device bf16 [sum_b len_b, Hkv, d]
- * (layout above).  len: host [B], len_b >= 0 (0 = request has no tokens in
+ * Eq. 14 merge into the running state).  k, v: device bf16 chunks in the
+ * round's kv_layout (token-major [sum_b len_b, Hkv, d] or head-major
+ * [Hkv, sum_b len_b, d]).  len: host [B], len_b >= 0 (0 = request has no tokens in
  * this chunk), sum <= max_chunk_tokens.  History tokens are visible to every
  * candidate query.  Chunks may come in any order and any number (>= 0),
  * before or after ss_attend_local_candidates.  If wait_before is non-null the
@@ -125,7 +138,10 @@ ss_status ss_attend_history_chunk(ss_round *r, const void *k, const void *v, con
 
 /* Attend the Speculative Frontier (paper Sec. 4.2, GPU-resident pass): query
  * i of request b sees candidate keys j <= i of the same request.  k_cand,
- * v_cand: device bf16 [sum n_b, Hkv, d].  Exactly once per round. */
+ * v_cand: device bf16 [sum n_b, Hkv, d].  Exactly once per round.  The pass
+ * is executed by the kernel ss_round_finalize enqueues (fused with the split
+ * merge and the normalisation), so k_cand and v_cand must stay valid and
+ * unchanged until finalize's work has completed; this call enqueues nothing. */
 ss_status ss_attend_local_candidates(ss_round *r, const void *k_cand, const void *v_cand,
                                      hipStream_t stream);
 
@@ -152,8 +168,9 @@ ss_status ss_pipeline_create(ss_pipeline **out, void *staging0, void *staging1, 
 /* Upload one history chunk into the next staging slot and attend it:
  *   copy_stream: wait free[s]; copy host_kv -> slot s; record ready[s]
  *   stream:      wait ready[s]; ss_attend_history_chunk; record free[s]
- * host_kv: pinned host bf16 [2][sum_b len_b][Hkv][d] (the chunk's K then its
- * V, contiguous), len as in ss_attend_history_chunk.  The chunk may belong
+ * host_kv: pinned host bf16, the chunk's K then its V, each in the round's
+ * kv_layout ([sum_b len_b][Hkv][d] or [Hkv][sum_b len_b][d]), contiguous;
+ * len as in ss_attend_history_chunk.  The chunk may belong
  * to any round (e.g. the next layer), so transfers run ahead across layer
  * boundaries. */
 ss_status ss_pipeline_attend_chunk(ss_pipeline *p, ss_round *r, const void *host_kv,

@@ -58,6 +58,8 @@ ss_status validate_desc(const ss_round_desc *d) {
     return fail(SS_ERR_INVALID_ARGUMENT, "split_tokens must be 0 or a positive multiple of %d", ss::kTile);
   if (d->mfma_min_rows < 0 || d->mfma_min_rows > ss::kMaxValuRows + 1)
     return fail(SS_ERR_INVALID_ARGUMENT, "mfma_min_rows must be in [0, %d]", ss::kMaxValuRows + 1);
+  if (d->kv_layout != SS_KV_TOKEN_MAJOR && d->kv_layout != SS_KV_HEAD_MAJOR)
+    return fail(SS_ERR_INVALID_ARGUMENT, "kv_layout must be SS_KV_TOKEN_MAJOR or SS_KV_HEAD_MAJOR");
   const int G = d->num_q_heads / d->num_kv_heads;
   long rows = 0;
   for (int b = 0; b < d->num_requests; ++b) {
@@ -85,9 +87,11 @@ size_t workspace_bytes_rows(long R) {
 struct ss_round {
   int32_t B, Hq, Hkv, G;
   float scale;
-  int32_t max_chunk_tokens, split_tokens, mfma_min_rows;
+  int32_t max_chunk_tokens, split_tokens, mfma_min_rows, kv_layout;
   std::vector<int32_t> n_cand, row_off;
+  std::vector<int32_t> slots_used;   // per request: state slots written so far this round
   const uint16_t *q;
+  const uint16_t *kc = nullptr, *vc = nullptr;   // candidate K/V, attended by finalize
   ss::State st;
   bool cand_done = false;
   bool finalized = false;
@@ -116,9 +120,14 @@ ss_status check_history_args(const ss_round *r, const int32_t *len, long *total)
   ss_status s = check_round(r);
   if (s != SS_OK) return s;
   if (len == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "len is null");
+  // an item must stay below 2^31 bytes of one KV head (32-bit buffer offsets)
+  const long max_piece = r->kv_layout == SS_KV_TOKEN_MAJOR ? ((1L << 31) - 512) / ((long)r->Hkv * 256)
+                                                           : ((1L << 31) - 512) / 256;
   long t = 0;
   for (int b = 0; b < r->B; ++b) {
     if (len[b] < 0) return fail(SS_ERR_INVALID_ARGUMENT, "len[%d] = %d < 0", b, len[b]);
+    if ((long)len[b] > max_piece / ss::kTile * ss::kTile * ss::kNumSlots)
+      return fail(SS_ERR_INVALID_ARGUMENT, "len[%d] = %d tokens is too large for one history call", b, len[b]);
     t += len[b];
   }
   if (t > r->max_chunk_tokens)
@@ -146,6 +155,9 @@ void plan_chunk(const ss_round *r, const int32_t *len, long total, Plan *plan) {
   }
   const long min_piece = align_up((max_len + ss::kNumSlots - 1) / ss::kNumSlots, ss::kTile);
   piece = std::max(piece, min_piece);
+  const long max_piece = r->kv_layout == SS_KV_TOKEN_MAJOR ? ((1L << 31) - 512) / ((long)r->Hkv * 256)
+                                                           : ((1L << 31) - 512) / 256;
+  piece = std::min(piece, max_piece / ss::kTile * ss::kTile);
   const int min_rows = r->mfma_min_rows > 0 ? r->mfma_min_rows : kDefaultMfmaMinRows;
   long off = 0;
   for (int b = 0; b < r->B; ++b) {
@@ -160,7 +172,7 @@ void plan_chunk(const ss_round *r, const int32_t *len, long total, Plan *plan) {
       it.tok_count = (int32_t)std::min<long>(piece, n - p0);
       it.q_row0 = r->row_off[b];
       it.n_cand = (int16_t)r->n_cand[b];
-      it.slot = (int16_t)slot;
+      it.slot = (int16_t)(slot | (slot >= r->slots_used[b] ? ss::kSlotFresh : 0));
       dst->push_back(it);
     }
     off += n;
@@ -172,7 +184,7 @@ void plan_chunk(const ss_round *r, const int32_t *len, long total, Plan *plan) {
   std::stable_sort(plan->rb2.begin(), plan->rb2.end(), by_len);
 }
 
-ss::ChunkParams *base_params(const ss_round *r, const void *k, const void *v) {
+ss::ChunkParams *base_params(const ss_round *r, const void *k, const void *v, long total) {
   static thread_local ss::ChunkParams p;
   p.k = static_cast<const uint16_t *>(k);
   p.v = static_cast<const uint16_t *>(v);
@@ -182,13 +194,20 @@ ss::ChunkParams *base_params(const ss_round *r, const void *k, const void *v) {
   p.Hkv = r->Hkv;
   p.G = r->G;
   p.scale_log2 = r->scale * 1.4426950408889634f;
+  if (r->kv_layout == SS_KV_TOKEN_MAJOR) {   // [sum len][Hkv][d]
+    p.tok_stride = (uint32_t)(r->Hkv * ss::kHeadDim);
+    p.head_stride = ss::kHeadDim;
+  } else {                                    // [Hkv][sum len][d]
+    p.tok_stride = ss::kHeadDim;
+    p.head_stride = (uint64_t)total * ss::kHeadDim;
+  }
   p.num_items = 0;
   return &p;
 }
 
 // Launch `items` in batches of kMaxItems with `launch(params)`.
-template <typename F>
-hipError_t launch_items(ss::ChunkParams *p, const std::vector<ss::Item> &items, F launch) {
+template <typename P, typename F>
+hipError_t launch_items(P *p, const std::vector<ss::Item> &items, F launch) {
   for (size_t i0 = 0; i0 < items.size(); i0 += ss::kMaxItems) {
     const size_t n = std::min<size_t>(ss::kMaxItems, items.size() - i0);
     std::memcpy(p->items, items.data() + i0, n * sizeof(ss::Item));
@@ -204,14 +223,19 @@ ss_status enqueue_history(ss_round *r, const void *k, const void *v, const int32
   if (total == 0) return SS_OK;
   Plan plan;
   plan_chunk(r, len, total, &plan);
-  ss::ChunkParams *p = base_params(r, k, v);
+  ss::ChunkParams *p = base_params(r, k, v, total);
   hipError_t e = launch_items(p, plan.rb2, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 2, stream); });
   if (e == hipSuccess)
     e = launch_items(p, plan.rb1, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 1, stream); });
   if (e == hipSuccess)
-    e = launch_items(p, plan.valu,
-                     [&](const ss::ChunkParams &q) { return ss::launch_chunk_valu(q, ss::kMaxValuRows, stream); });
+    e = launch_items(p, plan.valu, [&](const ss::ChunkParams &q) { return ss::launch_chunk_valu(q, stream); });
   if (e != hipSuccess) return hip_fail(e, "history chunk kernel launch");
+  // slots written by this call are valid from now on
+  for (const auto *lst : {&plan.valu, &plan.rb1, &plan.rb2})
+    for (const ss::Item &it : *lst) {
+      const int b = (int)(std::upper_bound(r->row_off.begin(), r->row_off.end(), it.q_row0) - r->row_off.begin()) - 1;
+      r->slots_used[b] = std::max(r->slots_used[b], (it.slot & 0xff) + 1);
+    }
   return SS_OK;
 }
 
@@ -266,11 +290,9 @@ ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q
   r->st.m = reinterpret_cast<float *>(ws + a_bytes);
   r->st.l = reinterpret_cast<float *>(ws + a_bytes + m_bytes);
   r->st.R = (int32_t)R;
-  const hipError_t e = ss::launch_init_state(r->st, stream);
-  if (e != hipSuccess) {
-    delete r;
-    return hip_fail(e, "state init launch");
-  }
+  r->kv_layout = desc->kv_layout;
+  r->slots_used.assign(r->B, 0);   // every slot starts empty: nothing to enqueue
+  (void)stream;
   *out = r;
   return SS_OK;
 }
@@ -325,17 +347,11 @@ ss_status ss_attend_local_candidates(ss_round *r, const void *k_cand, const void
   if (r->cand_done) return fail(SS_ERR_BAD_STATE, "local candidates already attended for this round");
   if (k_cand == nullptr || v_cand == nullptr || !aligned(k_cand, 16) || !aligned(v_cand, 16))
     return fail(SS_ERR_INVALID_ARGUMENT, "k_cand and v_cand must be non-null and 16-byte aligned");
-  std::vector<ss::Item> items(r->B);
-  for (int b = 0; b < r->B; ++b) {
-    items[b].tok_begin = 0;
-    items[b].tok_count = 0;
-    items[b].q_row0 = r->row_off[b];
-    items[b].n_cand = (int16_t)r->n_cand[b];
-    items[b].slot = 0;
-  }
-  ss::ChunkParams *p = base_params(r, k_cand, v_cand);
-  const hipError_t e = launch_items(p, items, [&](const ss::ChunkParams &q) { return ss::launch_candidates(q, stream); });
-  if (e != hipSuccess) return hip_fail(e, "candidate kernel launch");
+  // the frontier pass runs inside the finalize kernel (fused with the slot
+  // merge and the normalisation); the result does not depend on the order
+  (void)stream;
+  r->kc = static_cast<const uint16_t *>(k_cand);
+  r->vc = static_cast<const uint16_t *>(v_cand);
   r->cand_done = true;
   return SS_OK;
 }
@@ -346,7 +362,26 @@ ss_status ss_round_finalize(ss_round *r, float *out, float *lse, hipStream_t str
   if (!r->cand_done) return fail(SS_ERR_BAD_STATE, "finalize before ss_attend_local_candidates");
   if (out == nullptr || !aligned(out, 16)) return fail(SS_ERR_INVALID_ARGUMENT, "out must be non-null and 16-byte aligned");
   if (lse != nullptr && !aligned(lse, 4)) return fail(SS_ERR_INVALID_ARGUMENT, "lse must be 4-byte aligned");
-  const hipError_t e = ss::launch_finalize(r->st, out, lse, stream);
+  static thread_local ss::FinalParams p;
+  p.kc = r->kc;
+  p.vc = r->vc;
+  p.q = r->q;
+  p.out = out;
+  p.lse = lse;
+  p.st = r->st;
+  p.Hq = r->Hq;
+  p.Hkv = r->Hkv;
+  p.G = r->G;
+  p.scale_log2 = r->scale * 1.4426950408889634f;
+  std::vector<ss::Item> items(r->B);
+  for (int b = 0; b < r->B; ++b) {
+    items[b].tok_begin = 0;
+    items[b].tok_count = r->slots_used[b];
+    items[b].q_row0 = r->row_off[b];
+    items[b].n_cand = (int16_t)r->n_cand[b];
+    items[b].slot = 0;
+  }
+  const hipError_t e = launch_items(&p, items, [&](const ss::FinalParams &q) { return ss::launch_finalize(q, stream); });
   if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
   r->finalized = true;
   return SS_OK;

@@ -15,22 +15,30 @@ constexpr int kMaxCand = 8;         // candidates per request (k_b + 1)
 constexpr int kMaxValuRows = 4;     // rows per KV head the VALU chunk kernel handles
 constexpr int kMaxRows = 32;        // rows per KV head the MFMA chunk kernel handles
 
-// One workgroup's share of a history chunk for one request (x all KV heads
-// through blockIdx.y): tokens [tok_begin, tok_begin + tok_count) of the packed
-// chunk, folded into split slot `slot` of the request's query rows.
+// Item flag: the slot has not been written in this round yet, so the kernel
+// stores its result instead of merging with (uninitialised) workspace.
+constexpr int kSlotFresh = 0x100;
+
+// History item: one workgroup's share of a chunk for one request (x all KV
+// heads through blockIdx.y): tokens [tok_begin, tok_begin + tok_count) of
+// the packed chunk, folded into split slot (slot & 0xff) of the request's
+// query rows.
+// Finalize item: one request; tok_count = number of slots written by
+// history calls (slots >= that are empty), tok_begin unused.
 struct Item {
   int32_t tok_begin;
   int32_t tok_count;
   int32_t q_row0;   // off_b: first packed candidate row of the request
   int16_t n_cand;   // n_b
-  int16_t slot;
+  int16_t slot;     // slot index | kSlotFresh
 };
 static_assert(sizeof(Item) == 16, "Item layout");
 
 // Running state in the workspace, per slot s and query row R_idx = (off_b+i)*Hq+h:
-//   m[s*R + R_idx]   running max of sigma*log2(e)*q.k (log2 domain), -inf = empty
+//   m[s*R + R_idx]   running max of sigma*log2(e)*q.k (log2 domain)
 //   l[s*R + R_idx]   running sum of 2^(x - m)
 //   a[(s*R + R_idx)*d + c]  running weighted value sum (same scale as l)
+// A slot is valid only once a history item has written it in this round.
 struct State {
   float *m;
   float *l;
@@ -39,23 +47,35 @@ struct State {
 };
 
 struct ChunkParams {
-  const uint16_t *k;    // bf16 [sum len, Hkv, d]
+  const uint16_t *k;    // bf16 chunk: token-major [sum len][Hkv][d] or head-major [Hkv][sum len][d]
   const uint16_t *v;
   const uint16_t *q;    // bf16 [sum n_b, Hq, d]
   State st;
   int32_t Hq, Hkv, G;
   float scale_log2;     // softmax_scale * log2(e)
+  uint32_t tok_stride;  // elements between consecutive tokens of one KV head
+  uint64_t head_stride; // elements between KV heads at the same token
+  int32_t num_items;
+  Item items[kMaxItems];
+};
+
+struct FinalParams {
+  const uint16_t *kc;   // bf16 candidate K [sum n_b, Hkv, d]
+  const uint16_t *vc;   // bf16 candidate V
+  const uint16_t *q;
+  float *out;           // fp32 [sum n_b, Hq, d]
+  float *lse;           // fp32 [sum n_b, Hq] or null
+  State st;
+  int32_t Hq, Hkv, G;
+  float scale_log2;
   int32_t num_items;
   Item items[kMaxItems];
 };
 
 // Launch wrappers; return hipGetLastError() of the launch.
-hipError_t launch_init_state(const State &st, hipStream_t s);
 hipError_t launch_chunk_mfma(const ChunkParams &p, int row_blocks, hipStream_t s);
-hipError_t launch_chunk_valu(const ChunkParams &p, int max_rows, hipStream_t s);
-// Candidates: p.k / p.v are the candidate K / V [sum n_b, Hkv, d]; one item per
-// request (q_row0, n_cand; token fields unused), merged into slot 0.
-hipError_t launch_candidates(const ChunkParams &p, hipStream_t s);
-hipError_t launch_finalize(const State &st, float *out, float *lse, hipStream_t s);
+hipError_t launch_chunk_valu(const ChunkParams &p, hipStream_t s);
+// Speculative Frontier pass fused with the split-slot merge and O = a / l.
+hipError_t launch_finalize(const FinalParams &p, hipStream_t s);
 
 }  // namespace ss

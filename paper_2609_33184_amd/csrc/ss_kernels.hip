@@ -34,6 +34,7 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr int kAwPitch = 132;  // floats per row of a wave's partial accumulator
+constexpr int kBufferFlags = 0x00020000;   // buffer resource word 3: 32-bit data format, raw offsets
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -118,10 +119,9 @@ __device__ __forceinline__ void fold_into_slot(const ChunkParams &p, const Item 
       a[c + 3] += f[w] * x[3];
     }
   }
-  const size_t idx = (size_t)it.slot * p.st.R + global_row(p, it, g, r);
+  const size_t idx = (size_t)(it.slot & 0xff) * p.st.R + global_row(p, it, g, r);
   float *ap = p.st.a + idx * kHeadDim + seg * SEGLEN;
-  const float ms = p.st.m[idx];
-  if (ms == kNegInf) {               // empty slot: empty (+) X = X, old a is not read
+  if (it.slot & kSlotFresh) {        // first write of this slot in the round: store
 #pragma unroll
     for (int c = 0; c < SEGLEN; c += 4)
       *reinterpret_cast<f32x4_t *>(ap + c) = f32x4_t{a[c], a[c + 1], a[c + 2], a[c + 3]};
@@ -130,6 +130,7 @@ __device__ __forceinline__ void fold_into_slot(const ChunkParams &p, const Item 
       p.st.l[idx] = lstar;
     }
   } else {
+    const float ms = p.st.m[idx];
     const float mn = fmaxf(ms, mstar);
     const float alpha = exp2_fast(ms - mn);
     const float beta = exp2_fast(mstar - mn);
@@ -152,12 +153,14 @@ __device__ __forceinline__ void fold_into_slot(const ChunkParams &p, const Item 
 // ---------------------------------------------------------------------------
 // MFMA chunk kernel.  Workgroup = (item, kv head); 4 waves; wave w takes the
 // 32-token tiles w, w+4, ... of the item.  Per tile:
-//   S^T[t][row] = K Q^T      v_mfma_f32_16x16x32_bf16, A = K (16 tokens x 32 d
-//                            from registers), B = Q^T (held in registers)
+//   K, V tiles -> LDS        coalesced 16-byte loads: one instruction reads 4
+//                            whole 256-byte token rows (16 lanes per row)
+//   S^T[t][row] = K Q^T      v_mfma_f32_16x16x32_bf16, A = K (16 tokens x 32 d,
+//                            one ds_read_b128 per k-step), B = Q^T (from an
+//                            LDS copy of the group's query rows)
 //   online softmax per row   (row = lane % 16; the four lane groups share it)
-//   O^T[d][row] += V^T P^T   A = V^T read from a row-major LDS tile with the
-//                            LDS transpose read, B = P^T straight from the S
-//                            accumulators (hi and lo parts)
+//   O^T[d][row] += V^T P^T   A = V^T via the LDS transpose read, B = P^T
+//                            straight from the S accumulators (hi and lo parts)
 // Lane l: lr = l % 16, lq = l / 16.  In the S tile lane (lr, lq) holds
 // tokens 16u + 4*lq + r (u = 0,1; r = 0..3) of row lr; in O it holds
 // d = 16*db + 4*lq + r.  The reduction index of both MFMAs is permuted so
@@ -165,29 +168,37 @@ __device__ __forceinline__ void fold_into_slot(const ChunkParams &p, const Item 
 // d-chunk 4*s + lq (8 values); for PV lane group lq covers tokens
 // {4lq..4lq+3, 16+4lq..16+4lq+3}, exactly the S values the lane holds.
 //
+// LDS tiles are 32 rows of 256 bytes; 16-byte chunk c of token row t is
+// stored at chunk position c ^ (t & 15) for K and c ^ 2(t & 7) for V, which
+// makes the row-wise stores, the K operand reads (16 rows, same chunk) and
+// the transpose reads of V (8 rows, 32 bytes each per half-wave) free of
+// bank conflicts.
+//
 // ds_read_b64_tr_b16: within each 16-lane group, result lane i, element e is
 // element (i % 4) of what source lane 4e + i/4 addressed.  Source lane j of
 // group lq addresses row 4lq + j/4 (+16 for the second half), columns
 // 16db + 4(j%4) .. +3, so result lane i receives V[4lq + e][16db + i].
 //
-// Each wave keeps the next tile's K and V in flight in registers: K(i+1) is
-// issued as soon as S(i) has consumed K(i), V(i+1) as soon as V(i) is staged
-// in LDS, so at the top of an iteration only K is waited for.  The last tile
-// is peeled so the in-loop prefetch is unconditional (a conditional load
-// would make the compiler wait for every outstanding load).
+// Each wave keeps the next tile's K and V in flight in registers for the
+// whole compute of the current tile: a tile's loads are written to LDS at
+// the top of the iteration and the next loads are issued right after.  The
+// last tile is peeled so the in-loop prefetch is unconditional (a
+// conditional load would make the compiler wait for every outstanding load).
 // ---------------------------------------------------------------------------
-constexpr int kVPitch = 144;   // bf16 per LDS V row (128 + 16): rows 288 B apart
+constexpr int kRowBytes = kHeadDim * 2;          // 256
+constexpr int kTileBytes = kTile * kRowBytes;    // 8 KiB per K or V tile
 
 template <int RB>
 struct MfmaLds {
-  static constexpr int kVBytes = kWaves * kTile * kVPitch * 2;
+  static constexpr int kQBytes = RB * 16 * kRowBytes;               // Q rows, shared by the waves
+  static constexpr int kStageBytes = kQBytes + kWaves * 2 * kTileBytes;
   static constexpr int kMergeBytes = kWaves * RB * 16 * (kAwPitch + 2) * 4;
-  static constexpr int kBytes = kVBytes > kMergeBytes ? kVBytes : kMergeBytes;
+  static constexpr int kBytes = kStageBytes > kMergeBytes ? kStageBytes : kMergeBytes;
 };
 
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ s16x4_t lds_read_tr16(const uint16_t *p) {
+__device__ __forceinline__ s16x4_t lds_read_tr16(const unsigned char *p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
       (__attribute__((address_space(3))) s16x4_t *)(reinterpret_cast<uintptr_t>(p)));
 }
@@ -195,7 +206,7 @@ __device__ __forceinline__ s16x4_t lds_read_tr16(const uint16_t *p) {
 template <int RB>
 __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[MfmaLds<RB>::kBytes];
-  const int w = threadIdx.x >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15;
   const int lq = lane >> 4;
@@ -203,21 +214,6 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   const int g = blockIdx.y;
   const int M = it.n_cand * p.G;
   const int count = it.tok_count;
-
-  // Q^T operand: B[k = d][j = row]; lane (lr, lq), k-step s -> row lr, d-chunk 4s+lq
-  bf16x8_t qop[RB][4];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int r = rb * 16 + lr;
-    if (r < M) {
-      const u32x4_t *qp = reinterpret_cast<const u32x4_t *>(p.q + (size_t)global_row(p, it, g, r) * kHeadDim);
-#pragma unroll
-      for (int s = 0; s < 4; ++s) qop[rb][s] = __builtin_bit_cast(bf16x8_t, qp[4 * s + lq]);
-    } else {
-#pragma unroll
-      for (int s = 0; s < 4; ++s) qop[rb][s] = __builtin_bit_cast(bf16x8_t, u32x4_t{0, 0, 0, 0});
-    }
-  }
 
   float m_run[RB], l_run[RB];
   f32x4_t acc[RB][8];
@@ -229,51 +225,75 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
     for (int db = 0; db < 8; ++db) acc[rb][db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  // 32-bit element offsets inside the item (the host keeps an item < 2^30 elements)
-  const uint32_t tok_stride = (uint32_t)p.Hkv * kHeadDim;
-  const uint16_t *kbase = p.k + ((size_t)it.tok_begin * p.Hkv + g) * kHeadDim;
-  const uint16_t *vbase = p.v + ((size_t)it.tok_begin * p.Hkv + g) * kHeadDim;
-  uint16_t *vs = reinterpret_cast<uint16_t *>(smem) + w * (kTile * kVPitch);
+  // Buffer resources over this item's rows of KV head g: loads of tokens past
+  // the item return zero (their scores are masked), so no clamping is needed.
+  // Offsets are 32-bit (the host keeps an item below 2^31 bytes).
+  const uint32_t stride_b = p.tok_stride * 2;                      // bytes between tokens
+  const uint32_t nrec = (uint32_t)(count - 1) * stride_b + kRowBytes;
+  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride;
+  const __amdgpu_buffer_rsrc_t krs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k + first), (short)0, (int)nrec, kBufferFlags);
+  const __amdgpu_buffer_rsrc_t vrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v + first), (short)0, (int)nrec, kBufferFlags);
+  const uint32_t voff = lq * stride_b + 16 * lr;                     // token lq, chunk lr
+  unsigned char *qs = smem;
+  unsigned char *ks = smem + MfmaLds<RB>::kQBytes + w * (2 * kTileBytes);
+  unsigned char *vs = ks + kTileBytes;
   const int ntiles = (count + kTile - 1) / kTile;
   const float sl2 = p.scale_log2;
 
-  u32x4_t kr[2][4];
-  u32x4_t vr[8];
-  auto load_k = [&](int tb) {
+  u32x4_t kr[8], vr[8];
+  // coalesced loads: instruction i reads tokens tb + 4i + lq, chunk lr
+  auto load_kv = [&](int tb) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const uint32_t t = (uint32_t)min(tb + 16 * u + lr, count - 1);
-      const u32x4_t *src = reinterpret_cast<const u32x4_t *>(kbase + t * tok_stride);
+    for (int i = 0; i < 8; ++i)
+      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(krs, voff, (uint32_t)(tb + 4 * i) * stride_b, 0);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) kr[u][s] = src[4 * s + lq];
-    }
+    for (int i = 0; i < 8; ++i)
+      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, voff, (uint32_t)(tb + 4 * i) * stride_b, 0);
   };
-  auto load_v = [&](int tb) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const uint32_t t = (uint32_t)min(tb + 4 * i + lq, count - 1);
-      vr[i] = reinterpret_cast<const u32x4_t *>(vbase + t * tok_stride)[lr];
-    }
-  };
-  // V operand read addresses (row 4lq + lr/4, column 4*(lr%4)), first half
-  const uint16_t *vrd = vs + (4 * lq + (lr >> 2)) * kVPitch + 4 * (lr & 3);
+  // K operand read: row 16u + lr, chunk 4s + lq at position (4s + lq) ^ lr
+  // V transpose read: row 4lq + lr/4 (+16), chunk 2db + (lr&3)/2, half lr&1
+  const int vrow = 4 * lq + (lr >> 2);
+  const int vrd = vrow * kRowBytes + 8 * (lr & 1);
+  const int vsw = 2 * (vrow & 7);
+  const int vc0 = (lr & 3) >> 1;
 
   auto tile = [&](int tb, auto prefetch) {
     constexpr bool kPrefetch = decltype(prefetch)::value;
+    // stage K(i), V(i) in LDS, then issue the loads of the next tile
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int t = 4 * i + lq;
+      *reinterpret_cast<u32x4_t *>(ks + t * kRowBytes + 16 * (lr ^ (t & 15))) = kr[i];
+      *reinterpret_cast<u32x4_t *>(vs + t * kRowBytes + 16 * (lr ^ (2 * (t & 7)))) = vr[i];
+    }
+    if constexpr (kPrefetch) load_kv(tb + kWaves * kTile);
+    __builtin_amdgcn_sched_barrier(0);   // keep the prefetch here, ahead of the math
+
     // S^T = K Q^T
     f32x4_t sacc[2][RB];
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int u = 0; u < 2; ++u) {
+      bf16x8_t kop[4];
+      const int t = 16 * u + lr;
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        kop[s] = *reinterpret_cast<const bf16x8_t *>(ks + t * kRowBytes + 16 * ((4 * s + lq) ^ lr));
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         f32x4_t c = {0.f, 0.f, 0.f, 0.f};
+        const unsigned char *qrow = qs + (16 * rb + lr) * kRowBytes;
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
-          c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[u][s]), qop[rb][s], c, 0, 0, 0);
+        for (int s = 0; s < 4; ++s) {
+          const bf16x8_t qop = *reinterpret_cast<const bf16x8_t *>(qrow + 16 * ((4 * s + lq) ^ lr));
+          c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[s], qop, c, 0, 0, 0);
+        }
         sacc[u][rb] = c;
       }
-    if constexpr (kPrefetch) load_k(tb + kWaves * kTile);
-    __builtin_amdgcn_sched_barrier(0);   // keep the prefetch here, ahead of the softmax
+    }
+
+    __builtin_amdgcn_sched_barrier(0);   // phases stay apart: bounded register pressure
 
     // online softmax (Eq. 13 local terms merged per Eq. 14 into the wave's state)
     bf16x8_t phi[RB], plo[RB];
@@ -310,18 +330,14 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
       for (int db = 0; db < 8; ++db) acc[rb][db] *= alpha;
     }
 
-    // V tile -> LDS, row-major (token 4i + lq, 16-byte chunk lr); then prefetch
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      *reinterpret_cast<u32x4_t *>(vs + (4 * i + lq) * kVPitch + 8 * lr) = vr[i];
-    if constexpr (kPrefetch) load_v(tb + kWaves * kTile);
-    __builtin_amdgcn_sched_barrier(0);   // keep the prefetch here, ahead of PV
+    __builtin_amdgcn_sched_barrier(0);
 
     // O^T += V^T P^T  (hi and lo parts of P)
 #pragma unroll
     for (int db = 0; db < 8; ++db) {
-      const s16x4_t v0 = lds_read_tr16(vrd + 16 * db);
-      const s16x4_t v1 = lds_read_tr16(vrd + 16 * kVPitch + 16 * db);
+      const int off = vrd + 16 * ((2 * db + vc0) ^ vsw);
+      const s16x4_t v0 = lds_read_tr16(vs + off);
+      const s16x4_t v1 = lds_read_tr16(vs + off + 16 * kRowBytes);
       const bf16x8_t vop = __builtin_bit_cast(
           bf16x8_t, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
@@ -332,10 +348,21 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
     }
   };
 
+  // first tile in flight before the query rows are staged
   int t0 = w;
+  if (t0 < ntiles) load_kv(t0 * kTile);
+  // Q rows of this (request, kv head) -> LDS, chunk c of row r at c ^ (r & 15);
+  // rows >= M are zero.  The Q^T operand (B[k = d][j = row]) of lane (lr, lq),
+  // k-step s, is row lr's d-chunk 4s + lq.
+  for (int c = threadIdx.x; c < RB * 16 * 16; c += 256) {
+    const int r = c >> 4, ch = c & 15;
+    u32x4_t v = {0, 0, 0, 0};
+    if (r < M) v = reinterpret_cast<const u32x4_t *>(p.q + (size_t)global_row(p, it, g, r) * kHeadDim)[ch];
+    *reinterpret_cast<u32x4_t *>(qs + r * kRowBytes + 16 * (ch ^ (r & 15))) = v;
+  }
+  __syncthreads();
+
   if (t0 < ntiles) {
-    load_k(t0 * kTile);   // same issue order as the loop body: K, then V
-    load_v(t0 * kTile);
     for (; t0 + kWaves < ntiles; t0 += kWaves) tile(t0 * kTile, std::integral_constant<bool, true>{});
     tile(t0 * kTile, std::integral_constant<bool, false>{});
   }
@@ -360,6 +387,7 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   __syncthreads();
   fold_into_slot<RB * 16>(p, it, g, M, aw, mw, lw);
 }
+
 // ---------------------------------------------------------------------------
 // VALU chunk kernel for sparse query groups (few rows per KV head): fp32 dot
 // products on the vector ALUs, exact fp32 softmax weights.  Lane l: d-chunk
@@ -370,7 +398,7 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
 template <int MAXR>
 __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
   __shared__ __attribute__((aligned(16))) float smem[kWaves * MAXR * (kAwPitch + 2)];
-  const int w = threadIdx.x >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int lane = threadIdx.x & 63;
   const int c = lane & 15;
   const int tg = lane >> 4;
@@ -402,35 +430,33 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
   }
-  const size_t tok_stride = (size_t)p.Hkv * kHeadDim;
-  const uint16_t *kbase = p.k + ((size_t)it.tok_begin * p.Hkv + g) * kHeadDim;
-  const uint16_t *vbase = p.v + ((size_t)it.tok_begin * p.Hkv + g) * kHeadDim;
+  const uint32_t stride_b = p.tok_stride * 2;
+  const uint32_t nrec = (uint32_t)(count - 1) * stride_b + 2 * kHeadDim;
+  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride;
+  const __amdgpu_buffer_rsrc_t krs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k + first), (short)0, (int)nrec, kBufferFlags);
+  const __amdgpu_buffer_rsrc_t vrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v + first), (short)0, (int)nrec, kBufferFlags);
+  const uint32_t voff = tg * stride_b + 16 * c;
   const int ntiles = (count + kTile - 1) / kTile;
   const float sl2 = p.scale_log2;
 
+  // coalesced loads (4 token rows per instruction); tokens past the item read 0
   u32x4_t kr[8], vr[8];
   auto load_k = [&](int tb) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int t = min(tb + 4 * i + tg, count - 1);
-      kr[i] = reinterpret_cast<const u32x4_t *>(kbase + (size_t)t * tok_stride)[c];
-    }
+    for (int i = 0; i < 8; ++i)
+      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(krs, voff, (uint32_t)(tb + 4 * i) * stride_b, 0);
   };
   auto load_v = [&](int tb) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int t = min(tb + 4 * i + tg, count - 1);
-      vr[i] = reinterpret_cast<const u32x4_t *>(vbase + (size_t)t * tok_stride)[c];
-    }
+    for (int i = 0; i < 8; ++i)
+      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, voff, (uint32_t)(tb + 4 * i) * stride_b, 0);
   };
-  int tile = w;
-  if (tile < ntiles) {
-    load_k(tile * kTile);
-    load_v(tile * kTile);
-  }
-  for (; tile < ntiles; tile += kWaves) {
-    const int tb = tile * kTile;
-    const bool more = tile + kWaves < ntiles;
+  // one tile per iteration; the next tile's K is issued after the scores, its
+  // V after the PV update; the last tile is peeled (unconditional prefetch)
+  auto tile = [&](int tb, auto prefetch) {
+    constexpr bool more = decltype(prefetch)::value;
     float x[8][MAXR];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -450,7 +476,7 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
         x[i][r] = valid ? d * sl2 : kNegInf;
       }
     }
-    if (more) load_k(tb + kWaves * kTile);
+    if constexpr (more) load_k(tb + kWaves * kTile);
 #pragma unroll
     for (int r = 0; r < MAXR; ++r) {
       float mx = kNegInf;
@@ -483,7 +509,14 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(x[i][r], vf[e], acc[r][e]);
     }
-    if (more) load_v(tb + kWaves * kTile);
+    if constexpr (more) load_v(tb + kWaves * kTile);
+  };
+  int t0 = w;
+  if (t0 < ntiles) {
+    load_k(t0 * kTile);
+    load_v(t0 * kTile);
+    for (; t0 + kWaves < ntiles; t0 += kWaves) tile(t0 * kTile, std::integral_constant<bool, true>{});
+    tile(t0 * kTile, std::integral_constant<bool, false>{});
   }
 
   // reduce over the token groups, partials -> LDS
@@ -513,122 +546,87 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Speculative Frontier: query i of request b sees candidate keys j <= i.
-// Workgroup = (request, kv head); wave w takes rows w, w+4, ...; lane l holds
-// d = 2l, 2l+1.  The local state is merged into slot 0 (Eq. 14).
+// Finalize: for every query row (request b, candidate i, head h)
+//   * merge the split slots the history calls wrote (Eq. 14; slot count per
+//     request from the host, unwritten slots are never read),
+//   * attend the Speculative Frontier: candidate keys j <= i of the same
+//     request, causal by absolute position (Sec. 4.2, GPU-resident pass),
+//   * write O = a / l and LSE = m ln 2 + ln l (Eq. 17).
+// One wave per row (grid.y covers a request's rows, 4 per workgroup); lane l
+// holds d = 2l, 2l+1.  The <= 8 candidate dot products are reduced across
+// the wave as independent chains.
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) candidates_kernel(const ChunkParams p) {
+__global__ void __launch_bounds__(256) finalize_kernel(const FinalParams p) {
   const int w = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const Item it = p.items[blockIdx.x];
-  const int g = blockIdx.y;
-  const int n = it.n_cand;
-  const int M = n * p.G;
-  for (int r = w; r < M; r += kWaves) {
-    const int i = r / p.G;
-    const int row = global_row(p, it, g, r);
-    const uint32_t qw = reinterpret_cast<const uint32_t *>(p.q + (size_t)row * kHeadDim)[lane];
-    const float q0 = bf16_lo(qw), q1 = bf16_hi(qw);
-    float x[kMaxCand];
-    float mx = kNegInf;
+  const int r = blockIdx.y * kWaves + w;          // local row = i * Hq + h
+  if (r >= it.n_cand * p.Hq) return;
+  const int i = r / p.Hq;
+  const int h = r - i * p.Hq;
+  const int g = h / p.G;
+  const int row = it.q_row0 * p.Hq + r;           // (off_b + i) * Hq + h
+  const int nslot = it.tok_count;
+
+  const uint32_t qw = reinterpret_cast<const uint32_t *>(p.q + (size_t)row * kHeadDim)[lane];
+  const float q0 = bf16_lo(qw), q1 = bf16_hi(qw);
+  float x[kMaxCand];
+  uint32_t vw[kMaxCand];
 #pragma unroll
-    for (int j = 0; j < kMaxCand; ++j) {
-      x[j] = kNegInf;
-      if (j <= i) {
-        const size_t krow = ((size_t)(it.q_row0 + j) * p.Hkv + g) * kHeadDim;
-        const uint32_t kw = reinterpret_cast<const uint32_t *>(p.k + krow)[lane];
-        float d = fmaf(q0, bf16_lo(kw), q1 * bf16_hi(kw));
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) d += __shfl_xor(d, off);
-        x[j] = d * p.scale_log2;
-        mx = fmaxf(mx, x[j]);
-      }
-    }
-    float l = 0.f, a0 = 0.f, a1 = 0.f;
-#pragma unroll
-    for (int j = 0; j < kMaxCand; ++j) {
-      if (j <= i) {
-        const float pj = exp2_fast(x[j] - mx);
-        const size_t vrow = ((size_t)(it.q_row0 + j) * p.Hkv + g) * kHeadDim;
-        const uint32_t vw = reinterpret_cast<const uint32_t *>(p.v + vrow)[lane];
-        l += pj;
-        a0 = fmaf(pj, bf16_lo(vw), a0);
-        a1 = fmaf(pj, bf16_hi(vw), a1);
-      }
-    }
-    const size_t idx = (size_t)row;          // slot 0
-    float *ap = p.st.a + idx * kHeadDim + 2 * lane;
-    const float ms = p.st.m[idx];
-    if (ms == kNegInf) {
-      ap[0] = a0;
-      ap[1] = a1;
-      if (lane == 0) {
-        p.st.m[idx] = mx;
-        p.st.l[idx] = l;
-      }
-    } else {
-      const float mn = fmaxf(ms, mx);
-      const float alpha = exp2_fast(ms - mn);
-      const float beta = exp2_fast(mx - mn);
-      ap[0] = alpha * ap[0] + beta * a0;
-      ap[1] = alpha * ap[1] + beta * a1;
-      if (lane == 0) {
-        p.st.m[idx] = mn;
-        p.st.l[idx] = alpha * p.st.l[idx] + beta * l;
-      }
+  for (int j = 0; j < kMaxCand; ++j) {
+    x[j] = 0.f;
+    vw[j] = 0;
+    if (j <= i) {
+      const size_t kv = ((size_t)(it.q_row0 + j) * p.Hkv + g) * kHeadDim;
+      const uint32_t kw = reinterpret_cast<const uint32_t *>(p.kc + kv)[lane];
+      vw[j] = reinterpret_cast<const uint32_t *>(p.vc + kv)[lane];
+      x[j] = fmaf(q0, bf16_lo(kw), q1 * bf16_hi(kw));
     }
   }
-}
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1)
+#pragma unroll
+    for (int j = 0; j < kMaxCand; ++j) x[j] += __shfl_xor(x[j], off);
 
-// ---------------------------------------------------------------------------
-// Split-KV state merge + normalisation: for each query row merge the
-// kNumSlots slot states (Eq. 14; empty slots have weight 0) and write
-// O = a / l and LSE = m ln 2 + ln l.  One wave per row, lane l holds d = 2l, 2l+1.
-// ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) finalize_kernel(const State st, float *out, float *lse) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (row >= st.R) return;
-  float ms[kNumSlots];
   float mstar = kNegInf;
 #pragma unroll
+  for (int j = 0; j < kMaxCand; ++j) {
+    x[j] = j <= i ? x[j] * p.scale_log2 : kNegInf;
+    mstar = fmaxf(mstar, x[j]);
+  }
+  float ms[kNumSlots];
+#pragma unroll
   for (int s = 0; s < kNumSlots; ++s) {
-    ms[s] = st.m[(size_t)s * st.R + row];
+    ms[s] = s < nslot ? p.st.m[(size_t)s * p.st.R + row] : kNegInf;
     mstar = fmaxf(mstar, ms[s]);
   }
   float l = 0.f, a0 = 0.f, a1 = 0.f;
 #pragma unroll
   for (int s = 0; s < kNumSlots; ++s) {
-    if (ms[s] != kNegInf) {
-      const size_t idx = (size_t)s * st.R + row;
+    if (s < nslot) {
+      const size_t idx = (size_t)s * p.st.R + row;
       const float f = exp2_fast(ms[s] - mstar);
-      const float2 a = reinterpret_cast<const float2 *>(st.a + idx * kHeadDim)[lane];
-      l += f * st.l[idx];
+      const float2 a = reinterpret_cast<const float2 *>(p.st.a + idx * kHeadDim)[lane];
+      l = fmaf(f, p.st.l[idx], l);
       a0 = fmaf(f, a.x, a0);
       a1 = fmaf(f, a.y, a1);
     }
   }
-  const float inv = 1.0f / l;
-  reinterpret_cast<float2 *>(out + (size_t)row * kHeadDim)[lane] = make_float2(a0 * inv, a1 * inv);
-  if (lse != nullptr && lane == 0) lse[row] = mstar * 0.69314718055994531f + logf(l);
-}
-
-__global__ void init_state_kernel(const State st) {
-  const size_t n = (size_t)kNumSlots * st.R;
-  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
-    st.m[i] = kNegInf;
-    st.l[i] = 0.f;
+#pragma unroll
+  for (int j = 0; j < kMaxCand; ++j) {
+    if (j <= i) {
+      const float pj = exp2_fast(x[j] - mstar);
+      l += pj;
+      a0 = fmaf(pj, bf16_lo(vw[j]), a0);
+      a1 = fmaf(pj, bf16_hi(vw[j]), a1);
+    }
   }
+  const float inv = 1.0f / l;
+  reinterpret_cast<float2 *>(p.out + (size_t)row * kHeadDim)[lane] = make_float2(a0 * inv, a1 * inv);
+  if (p.lse != nullptr && lane == 0) p.lse[row] = mstar * 0.69314718055994531f + logf(l);
 }
 
 }  // namespace
-
-hipError_t launch_init_state(const State &st, hipStream_t s) {
-  const size_t n = (size_t)kNumSlots * st.R;
-  const int blocks = (int)((n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048);
-  hipLaunchKernelGGL(init_state_kernel, dim3(blocks), dim3(256), 0, s, st);
-  return hipGetLastError();
-}
 
 hipError_t launch_chunk_mfma(const ChunkParams &p, int row_blocks, hipStream_t s) {
   const dim3 grid(p.num_items, p.Hkv);
@@ -639,20 +637,15 @@ hipError_t launch_chunk_mfma(const ChunkParams &p, int row_blocks, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_chunk_valu(const ChunkParams &p, int max_rows, hipStream_t s) {
-  const dim3 grid(p.num_items, p.Hkv);
-  (void)max_rows;  // rows per KV head <= kMaxValuRows, checked by the host
-  hipLaunchKernelGGL(chunk_attn_valu<kMaxValuRows>, grid, dim3(256), 0, s, p);
+hipError_t launch_chunk_valu(const ChunkParams &p, hipStream_t s) {
+  hipLaunchKernelGGL(chunk_attn_valu<kMaxValuRows>, dim3(p.num_items, p.Hkv), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
-hipError_t launch_candidates(const ChunkParams &p, hipStream_t s) {
-  hipLaunchKernelGGL(candidates_kernel, dim3(p.num_items, p.Hkv), dim3(256), 0, s, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_finalize(const State &st, float *out, float *lse, hipStream_t s) {
-  hipLaunchKernelGGL(finalize_kernel, dim3((st.R + 3) / 4), dim3(256), 0, s, st, out, lse);
+hipError_t launch_finalize(const FinalParams &p, hipStream_t s) {
+  int rows = 0;
+  for (int i = 0; i < p.num_items; ++i) rows = rows > p.items[i].n_cand * p.Hq ? rows : p.items[i].n_cand * p.Hq;
+  hipLaunchKernelGGL(finalize_kernel, dim3(p.num_items, (rows + kWaves - 1) / kWaves), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

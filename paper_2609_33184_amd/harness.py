@@ -19,7 +19,8 @@ class RoundBuffers:
     """Queries, candidate K/V, workspace and outputs of one layer's round."""
 
     def __init__(self, w: Workload, layer: int = 0, device="cuda", split_tokens: int = 0,
-                 mfma_min_rows: int = 0, max_chunk_tokens: Optional[int] = None):
+                 mfma_min_rows: int = 0, max_chunk_tokens: Optional[int] = None,
+                 kv_layout: int = ss.SS_KV_TOKEN_MAJOR):
         self.w = w
         self.layer = layer
         self.device = device
@@ -27,8 +28,9 @@ class RoundBuffers:
         self.kc = w.k_cand_all(layer, device)
         self.vc = w.v_cand_all(layer, device)
         mct = max_chunk_tokens or max(1, max(sum(w.chunk_lens(j)) for j in range(max(1, w.num_chunks))))
+        self.kv_layout = kv_layout
         self.desc = ss.make_desc(w.num_cand, w.num_q_heads, w.num_kv_heads, w.head_dim, w.softmax_scale,
-                                 mct, split_tokens, mfma_min_rows)
+                                 mct, split_tokens, mfma_min_rows, kv_layout)
         self.ws_bytes = ss.ss_round_workspace_bytes(self.desc)
         if self.ws_bytes == 0:
             raise ss.SpecStreamError(ss.SS_ERR_INVALID_ARGUMENT, "ss_round_workspace_bytes", ss.ss_last_error())
@@ -43,9 +45,12 @@ class RoundBuffers:
         self.q.copy_(self.w.q_all(layer, self.device))
 
 
-def hbm_history(w: Workload, layer: int = 0, device="cuda") -> List[Tuple[torch.Tensor, torch.Tensor]]:
-    """Every history chunk resident in device memory: [(k_j, v_j)]."""
-    return [w.chunk_kv(j, layer, device) for j in range(w.num_chunks)]
+def hbm_history(w: Workload, layer: int = 0, device="cuda", kv_layout: int = ss.SS_KV_TOKEN_MAJOR
+                ) -> List[Tuple[torch.Tensor, torch.Tensor]]:
+    """Every history chunk resident in device memory: [(k_j, v_j)] in the
+    given chunk layout."""
+    hm = kv_layout == ss.SS_KV_HEAD_MAJOR
+    return [w.chunk_kv(j, layer, device, head_major=hm) for j in range(w.num_chunks)]
 
 
 def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor]], stream: int,
@@ -73,11 +78,13 @@ def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor
 
 
 class HostHistory:
-    """One layer's history in pinned host memory, chunk j as [2][sum len_bj][Hkv][d]
-    (its K then its V), for streaming through the two-slot pipeline."""
+    """One layer's history in pinned host memory, chunk j as its K then its V
+    (each in the round's chunk layout), for streaming through the two-slot
+    pipeline."""
 
-    def __init__(self, w: Workload, layer: int = 0, gen_device="cuda"):
+    def __init__(self, w: Workload, layer: int = 0, gen_device="cuda", kv_layout: int = ss.SS_KV_TOKEN_MAJOR):
         self.w = w
+        hm = kv_layout == ss.SS_KV_HEAD_MAJOR
         tb = w.num_kv_heads * w.head_dim * BF16_BYTES
         self.sizes = [2 * sum(w.chunk_lens(j)) * tb for j in range(w.num_chunks)]
         self.offsets = []
@@ -90,7 +97,7 @@ class HostHistory:
         for j in range(w.num_chunks):
             if self.sizes[j] == 0:
                 continue
-            k, v = w.chunk_kv(j, layer, gen_device)
+            k, v = w.chunk_kv(j, layer, gen_device, head_major=hm)
             half = self.sizes[j] // 2
             o = self.offsets[j]
             self.buf[o:o + half].copy_(k.view(-1).view(torch.uint8).cpu())

@@ -24,6 +24,9 @@ SS_ERR_NOT_PINNED = -4
 SS_ERR_WORKSPACE = -5
 SS_ERR_HIP = -6
 
+SS_KV_TOKEN_MAJOR = 0   # history chunk [sum len][Hkv][d]
+SS_KV_HEAD_MAJOR = 1    # history chunk [Hkv][sum len][d]
+
 EXPORTED = (
     "ss_round_workspace_bytes", "ss_round_init", "ss_upload_chunk", "ss_attend_history_chunk",
     "ss_attend_local_candidates", "ss_round_finalize", "ss_round_destroy", "ss_pipeline_create",
@@ -49,18 +52,20 @@ class ss_round_desc(ctypes.Structure):
         ("max_chunk_tokens", ctypes.c_int32),
         ("split_tokens", ctypes.c_int32),
         ("mfma_min_rows", ctypes.c_int32),
+        ("kv_layout", ctypes.c_int32),
     ]
 
 
 def make_desc(num_cand: Sequence[int], num_q_heads: int, num_kv_heads: int, head_dim: int = 128,
               softmax_scale: Optional[float] = None, max_chunk_tokens: int = 1 << 30,
-              split_tokens: int = 0, mfma_min_rows: int = 0) -> ss_round_desc:
+              split_tokens: int = 0, mfma_min_rows: int = 0, kv_layout: int = SS_KV_TOKEN_MAJOR
+              ) -> ss_round_desc:
     """Build a descriptor; the candidate-count array is kept alive on it."""
     arr = (ctypes.c_int32 * len(num_cand))(*[int(x) for x in num_cand])
     d = ss_round_desc(len(num_cand), num_q_heads, num_kv_heads, head_dim,
                       (head_dim ** -0.5) if softmax_scale is None else softmax_scale,
                       ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)), max_chunk_tokens, split_tokens,
-                      mfma_min_rows)
+                      mfma_min_rows, kv_layout)
     d._keep = arr
     return d
 

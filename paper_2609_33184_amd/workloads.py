@@ -333,9 +333,13 @@ class Workload:
     def v_cand_all(self, layer: int = 0, device="cpu") -> torch.Tensor:
         return torch.cat([self.v_cand(b, layer=layer, device=device) for b in range(self.B)], 0)
 
-    def chunk_kv(self, j: int, layer: int = 0, device="cpu", out_k=None, out_v=None
+    def chunk_kv(self, j: int, layer: int = 0, device="cpu", out_k=None, out_v=None, head_major: bool = False
                  ) -> Tuple[torch.Tensor, torch.Tensor]:
-        """History chunk j packed in request order: [sum_b len_bj, Hkv, d] each."""
+        """History chunk j packed in request order: [sum_b len_bj, Hkv, d] each
+        (token-major), or [Hkv, sum_b len_bj, d] with ``head_major``."""
+        if head_major:
+            k, v = self.chunk_kv(j, layer, device)
+            return k.transpose(0, 1).contiguous(), v.transpose(0, 1).contiguous()
         lens = self.chunk_lens(j)
         tot = sum(lens)
         shape = (tot, self.num_kv_heads, self.head_dim)

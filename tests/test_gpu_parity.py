@@ -28,9 +28,14 @@ def stream():
     torch.cuda.synchronize()
 
 
-def _run(w, stream, **kw):
-    b = H.RoundBuffers(w, split_tokens=kw.pop("split_tokens", 0), mfma_min_rows=kw.pop("mfma_min_rows", 0))
-    chunks = H.hbm_history(w)
+LAYOUTS = [ss.SS_KV_TOKEN_MAJOR, ss.SS_KV_HEAD_MAJOR]
+LAYOUT_IDS = ["token_major", "head_major"]
+
+
+def _run(w, stream, kv_layout=ss.SS_KV_TOKEN_MAJOR, **kw):
+    b = H.RoundBuffers(w, split_tokens=kw.pop("split_tokens", 0), mfma_min_rows=kw.pop("mfma_min_rows", 0),
+                       kv_layout=kv_layout)
+    chunks = H.hbm_history(w, kv_layout=kv_layout)
     torch.cuda.synchronize()
     H.run_round(b, chunks, stream.cuda_stream, **kw)
     stream.synchronize()
@@ -43,10 +48,11 @@ def _full_check(w, b, what):
     assert_parity(b.lse.double().cpu().numpy(), ref_l, what + " lse", max_abs=1e-3, rel_l2=1e-4)
 
 
-def test_config1_tiny_full(stream):
+@pytest.mark.parametrize("layout", LAYOUTS, ids=LAYOUT_IDS)
+def test_config1_tiny_full(stream, layout):
     w = W.workload(1)
-    print("config 1 tiny, in-HBM", flush=True)
-    b = _run(w, stream)
+    print(f"config 1 tiny, in-HBM, layout {layout}", flush=True)
+    b = _run(w, stream, kv_layout=layout)
     _full_check(w, b, "config1")
 
 
@@ -65,17 +71,19 @@ def test_config2_full(stream):
     _full_check(w, b, "config2")
 
 
-def test_config3_sampled_full_size(stream):
+@pytest.mark.parametrize("layout", LAYOUTS, ids=LAYOUT_IDS)
+def test_config3_sampled_full_size(stream, layout):
     w = W.workload(3)
-    print("config 3 (16 x 32768), in-HBM, bench launch configuration", flush=True)
-    b = _run(w, stream)
+    print(f"config 3 (16 x 32768), in-HBM, bench launch configuration, layout {layout}", flush=True)
+    b = _run(w, stream, kv_layout=layout)
     check_sampled(w, b.out, b.lse, [(0, 0), (7, 3), (15, 7)], what="config3")
 
 
-def test_config4_sampled_full_size(stream):
+@pytest.mark.parametrize("layout", LAYOUTS, ids=LAYOUT_IDS)
+def test_config4_sampled_full_size(stream, layout):
     w = W.workload(4)
-    print("config 4 (ragged 64), in-HBM", flush=True)
-    b = _run(w, stream)
+    print(f"config 4 (ragged 64), in-HBM, layout {layout}", flush=True)
+    b = _run(w, stream, kv_layout=layout)
     lens = np.array(w.hist_len)
     cands = np.array(w.num_cand)
     pick = {int(lens.argmax()), int(lens.argmin()), int(np.where(cands == 1)[0][0]),
@@ -86,8 +94,8 @@ def test_config4_sampled_full_size(stream):
 
 def test_config5_one_layer_full_size(stream):
     w = W.workload(5)
-    print("config 5 (32 x 131072, outliers), one layer in-HBM", flush=True)
-    b = _run(w, stream)
+    print("config 5 (32 x 131072, outliers), one layer in-HBM, head-major", flush=True)
+    b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR)
     check_sampled(w, b.out, b.lse, [(0, 1), (31, 6)], what="config5 layer0")
 
 
@@ -104,10 +112,11 @@ def test_small_edge_cases(stream):
     for k, (lens, cands, hq, hkv) in enumerate(cases):
         w = W.custom(lens, cands, num_q_heads=hq, num_kv_heads=hkv, chunk_tokens=256, seed_base=40 + k)
         for mfma_min_rows in (0, 1):
-            print(f"edge case {k}: lens={lens} cands={cands} Hq={hq} Hkv={hkv} mfma_min_rows={mfma_min_rows}",
-                  flush=True)
-            b = _run(w, stream, mfma_min_rows=mfma_min_rows)
-            _full_check(w, b, f"edge{k}/{mfma_min_rows}")
+            for layout in LAYOUTS:
+                print(f"edge case {k}: lens={lens} cands={cands} Hq={hq} Hkv={hkv} "
+                      f"mfma_min_rows={mfma_min_rows} layout={layout}", flush=True)
+                b = _run(w, stream, mfma_min_rows=mfma_min_rows, kv_layout=layout)
+                _full_check(w, b, f"edge{k}/{mfma_min_rows}/{layout}")
 
 
 def test_valu_and_mfma_paths_agree_with_oracle(stream):
