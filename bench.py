@@ -50,9 +50,9 @@ def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
 
 
-def time_round_steps(torch, H, b, chunks, stream, steps: int, warmup: int):
+def time_round_steps(torch, H, b, chunks, stream, steps: int, warmup: int, batch: int = 1):
     for _ in range(warmup):
-        H.run_round(b, chunks, stream.cuda_stream)
+        H.run_round(b, chunks, stream.cuda_stream, batch=batch)
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
@@ -60,7 +60,7 @@ def time_round_steps(torch, H, b, chunks, stream, steps: int, warmup: int):
     e0.record(stream)
     t0 = time.perf_counter()
     for _ in range(steps):
-        H.run_round(b, chunks, stream.cuda_stream)
+        H.run_round(b, chunks, stream.cuda_stream, batch=batch)
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -179,6 +179,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--split-tokens", type=int, default=0)
+    ap.add_argument("--batch", type=int, default=1,
+                    help="history chunks per ss_attend_history_chunks call in the timed round (1 = one call per chunk)")
     ap.add_argument("--kv-layout", choices=["token", "head"], default="head",
                     help="history chunk layout: token-major [tok][Hkv][d] or head-major [Hkv][tok][d]")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -227,7 +229,7 @@ def main() -> int:
         return 0
 
     log("bench: timed rounds")
-    dt, wall = time_round_steps(torch, H, b, chunks, stream, args.steps, args.warmup)
+    dt, wall = time_round_steps(torch, H, b, chunks, stream, args.steps, args.warmup, args.batch)
     step_s = dt / args.steps
     kv_bytes = w.algorithmic_kv_bytes()
     value = kv_bytes * args.steps / dt / 1e9

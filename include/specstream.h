@@ -136,6 +136,17 @@ ss_status ss_upload_chunk(void *dst_device, const void *src_pinned_host, size_t 
 ss_status ss_attend_history_chunk(ss_round *r, const void *k, const void *v, const int32_t *len,
                                   hipEvent_t wait_before, hipEvent_t signal_after, hipStream_t stream);
 
+/* Attend several history chunks in one launch (paper Sec. 4.2: adjacent
+ * chunks are grouped into batches to amortise submission, synchronisation
+ * and kernel-launch costs).  Same semantics as num_chunks calls of
+ * ss_attend_history_chunk, in any order.  k, v: host arrays [num_chunks] of
+ * device chunk pointers (each chunk in the round's kv_layout); len: host
+ * [num_chunks][B] token counts; 1 <= num_chunks <= 32.  wait_before and
+ * signal_after bracket the whole batch. */
+ss_status ss_attend_history_chunks(ss_round *r, int32_t num_chunks, const void *const *k,
+                                   const void *const *v, const int32_t *len, hipEvent_t wait_before,
+                                   hipEvent_t signal_after, hipStream_t stream);
+
 /* Attend the Speculative Frontier (paper Sec. 4.2, GPU-resident pass): query
  * i of request b sees candidate keys j <= i of the same request.  k_cand,
  * v_cand: device bf16 [sum n_b, Hkv, d].  Exactly once per round.  The pass

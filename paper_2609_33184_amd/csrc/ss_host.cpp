@@ -35,9 +35,10 @@ ss_status hip_fail(hipError_t e, const char *what) {
 inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Workgroups one history call aims for (2 resident per CU on 256 CUs).
+// Workgroups one history chunk aims for (2 resident per CU on 256 CUs).
 constexpr long kTargetWorkgroups = 512;
 constexpr int kMinPiece = 256;
+constexpr int kMaxAutoPiece = 2048;
 constexpr int kDefaultMfmaMinRows = ss::kMaxValuRows + 1;
 
 ss_status validate_desc(const ss_round_desc *d) {
@@ -115,91 +116,124 @@ ss_status check_round(const ss_round *r) {
   return SS_OK;
 }
 
-// Validate a history call's arguments; total tokens in *total.
-ss_status check_history_args(const ss_round *r, const int32_t *len, long *total) {
+long max_piece_tokens(const ss_round *r) {
+  // an item must stay below 2^31 bytes of one KV head (32-bit buffer offsets)
+  const long per_tok = r->kv_layout == SS_KV_TOKEN_MAJOR ? (long)r->Hkv * 2 * ss::kHeadDim : 2 * ss::kHeadDim;
+  return ((1L << 31) - 1024) / per_tok / ss::kTile * ss::kTile;
+}
+
+// Validate a (batched) history call; per-chunk totals in tot[c].
+ss_status check_history_args(const ss_round *r, int nchunks, const void *const *k, const void *const *v,
+                             const int32_t *len, std::vector<long> *tot) {
   ss_status s = check_round(r);
   if (s != SS_OK) return s;
+  if (nchunks < 1 || nchunks > ss::kMaxChunks)
+    return fail(SS_ERR_INVALID_ARGUMENT, "num_chunks = %d outside [1, %d]", nchunks, ss::kMaxChunks);
   if (len == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "len is null");
-  // an item must stay below 2^31 bytes of one KV head (32-bit buffer offsets)
-  const long max_piece = r->kv_layout == SS_KV_TOKEN_MAJOR ? ((1L << 31) - 512) / ((long)r->Hkv * 256)
-                                                           : ((1L << 31) - 512) / 256;
-  long t = 0;
-  for (int b = 0; b < r->B; ++b) {
-    if (len[b] < 0) return fail(SS_ERR_INVALID_ARGUMENT, "len[%d] = %d < 0", b, len[b]);
-    if ((long)len[b] > max_piece / ss::kTile * ss::kTile * ss::kNumSlots)
-      return fail(SS_ERR_INVALID_ARGUMENT, "len[%d] = %d tokens is too large for one history call", b, len[b]);
-    t += len[b];
+  const long cap = max_piece_tokens(r) * ss::kNumSlots;
+  tot->assign(nchunks, 0);
+  for (int c = 0; c < nchunks; ++c) {
+    long t = 0;
+    for (int b = 0; b < r->B; ++b) {
+      const int32_t n = len[(size_t)c * r->B + b];
+      if (n < 0) return fail(SS_ERR_INVALID_ARGUMENT, "len[%d][%d] = %d < 0", c, b, n);
+      if ((long)n > cap) return fail(SS_ERR_INVALID_ARGUMENT, "len[%d][%d] = %d is too large", c, b, n);
+      t += n;
+    }
+    if (t > r->max_chunk_tokens)
+      return fail(SS_ERR_INVALID_ARGUMENT, "chunk %d has %ld tokens > max_chunk_tokens %d", c, t, r->max_chunk_tokens);
+    if (t > 0 && (k == nullptr || v == nullptr || k[c] == nullptr || v[c] == nullptr || !aligned(k[c], 16) ||
+                  !aligned(v[c], 16)))
+      return fail(SS_ERR_INVALID_ARGUMENT, "chunk %d: k and v must be non-null and 16-byte aligned", c);
+    (*tot)[c] = t;
   }
-  if (t > r->max_chunk_tokens)
-    return fail(SS_ERR_INVALID_ARGUMENT, "chunk has %ld tokens > max_chunk_tokens %d", t, r->max_chunk_tokens);
-  *total = t;
   return SS_OK;
 }
 
 struct Plan {
   std::vector<ss::Item> valu, rb1, rb2;
+  std::vector<int32_t> slots_after;   // per request: slots in use after this call
 };
 
-// Split every request's tokens of this chunk into pieces of `piece` tokens;
-// piece p of a request folds into state slot p.
-void plan_chunk(const ss_round *r, const int32_t *len, long total, Plan *plan) {
-  int max_len = 0;
-  for (int b = 0; b < r->B; ++b) max_len = std::max(max_len, len[b]);
+// Split every request's tokens of every chunk into pieces of `piece` tokens;
+// the pieces of one request get distinct state slots 0, 1, ...
+ss_status plan_chunks(const ss_round *r, int nchunks, const int32_t *len, const std::vector<long> &tot,
+                      Plan *plan) {
+  long total = 0;
+  for (long t : tot) total += t;
   long piece;
   if (r->split_tokens > 0) {
     piece = r->split_tokens;
   } else {
-    const long work = total * r->Hkv;
-    piece = (work + kTargetWorkgroups - 1) / kTargetWorkgroups;
-    piece = std::max<long>(kMinPiece, align_up(piece, ss::kTile));
+    // ~512 workgroups for one chunk of a large Cohort, never pieces above
+    // kMaxAutoPiece (folds of the running state stay a few % of the KV bytes
+    // while batched launches get enough workgroups to balance the CUs)
+    const long per_chunk_work = (total / nchunks) * r->Hkv;
+    piece = (per_chunk_work + kTargetWorkgroups - 1) / kTargetWorkgroups;
+    piece = std::min<long>(kMaxAutoPiece, std::max<long>(kMinPiece, align_up(piece, ss::kTile)));
   }
-  const long min_piece = align_up((max_len + ss::kNumSlots - 1) / ss::kNumSlots, ss::kTile);
-  piece = std::max(piece, min_piece);
-  const long max_piece = r->kv_layout == SS_KV_TOKEN_MAJOR ? ((1L << 31) - 512) / ((long)r->Hkv * 256)
-                                                           : ((1L << 31) - 512) / 256;
-  piece = std::min(piece, max_piece / ss::kTile * ss::kTile);
+  const long pmax = max_piece_tokens(r);
+  piece = std::min(piece, pmax);
+  // every request must fit its pieces into the slots
+  for (;;) {
+    bool ok = true;
+    for (int b = 0; b < r->B && ok; ++b) {
+      long pieces = 0;
+      for (int c = 0; c < nchunks; ++c) pieces += (len[(size_t)c * r->B + b] + piece - 1) / piece;
+      ok = pieces <= ss::kNumSlots;
+    }
+    if (ok) break;
+    if (piece >= pmax) return fail(SS_ERR_INVALID_ARGUMENT, "too many tokens per request for one history call");
+    piece = std::min(pmax, piece * 2);
+  }
   const int min_rows = r->mfma_min_rows > 0 ? r->mfma_min_rows : kDefaultMfmaMinRows;
-  long off = 0;
+  plan->slots_after = r->slots_used;
+  std::vector<long> off(nchunks, 0);
   for (int b = 0; b < r->B; ++b) {
-    const int n = len[b];
     const int M = r->n_cand[b] * r->G;
     std::vector<ss::Item> *dst = (M < min_rows && M <= ss::kMaxValuRows) ? &plan->valu
                                  : (M <= 16)                             ? &plan->rb1
                                                                          : &plan->rb2;
-    for (long p0 = 0, slot = 0; p0 < n; p0 += piece, ++slot) {
-      ss::Item it;
-      it.tok_begin = (int32_t)(off + p0);
-      it.tok_count = (int32_t)std::min<long>(piece, n - p0);
-      it.q_row0 = r->row_off[b];
-      it.n_cand = (int16_t)r->n_cand[b];
-      it.slot = (int16_t)(slot | (slot >= r->slots_used[b] ? ss::kSlotFresh : 0));
-      dst->push_back(it);
+    int slot = 0;
+    for (int c = 0; c < nchunks; ++c) {
+      const long n = len[(size_t)c * r->B + b];
+      for (long p0 = 0; p0 < n; p0 += piece, ++slot) {
+        ss::Item it;
+        it.tok_begin = (int32_t)(off[c] + p0);
+        it.tok_count = (int32_t)std::min<long>(piece, n - p0);
+        it.q_row0 = r->row_off[b];
+        it.n_cand = (uint8_t)r->n_cand[b];
+        it.chunk = (uint8_t)c;
+        it.slot = (uint8_t)slot;
+        it.flags = slot >= r->slots_used[b] ? ss::kSlotFresh : 0;
+        dst->push_back(it);
+      }
+      off[c] += n;
     }
-    off += n;
+    plan->slots_after[b] = std::max(plan->slots_after[b], slot);
   }
   // longest pieces first (a partial piece never delays the tail of the grid)
   auto by_len = [](const ss::Item &a, const ss::Item &b) { return a.tok_count > b.tok_count; };
   std::stable_sort(plan->valu.begin(), plan->valu.end(), by_len);
   std::stable_sort(plan->rb1.begin(), plan->rb1.end(), by_len);
   std::stable_sort(plan->rb2.begin(), plan->rb2.end(), by_len);
+  return SS_OK;
 }
 
-ss::ChunkParams *base_params(const ss_round *r, const void *k, const void *v, long total) {
+ss::ChunkParams *base_params(const ss_round *r, int nchunks, const void *const *k, const void *const *v,
+                             const std::vector<long> &tot) {
   static thread_local ss::ChunkParams p;
-  p.k = static_cast<const uint16_t *>(k);
-  p.v = static_cast<const uint16_t *>(v);
   p.q = r->q;
   p.st = r->st;
   p.Hq = r->Hq;
   p.Hkv = r->Hkv;
   p.G = r->G;
   p.scale_log2 = r->scale * 1.4426950408889634f;
-  if (r->kv_layout == SS_KV_TOKEN_MAJOR) {   // [sum len][Hkv][d]
-    p.tok_stride = (uint32_t)(r->Hkv * ss::kHeadDim);
-    p.head_stride = ss::kHeadDim;
-  } else {                                    // [Hkv][sum len][d]
-    p.tok_stride = ss::kHeadDim;
-    p.head_stride = (uint64_t)total * ss::kHeadDim;
+  p.tok_stride = r->kv_layout == SS_KV_TOKEN_MAJOR ? (uint32_t)(r->Hkv * ss::kHeadDim) : ss::kHeadDim;
+  for (int c = 0; c < nchunks; ++c) {
+    p.k[c] = static_cast<const uint16_t *>(k[c]);
+    p.v[c] = static_cast<const uint16_t *>(v[c]);
+    p.head_stride[c] = r->kv_layout == SS_KV_TOKEN_MAJOR ? (uint64_t)ss::kHeadDim : (uint64_t)tot[c] * ss::kHeadDim;
   }
   p.num_items = 0;
   return &p;
@@ -218,24 +252,37 @@ hipError_t launch_items(P *p, const std::vector<ss::Item> &items, F launch) {
   return hipSuccess;
 }
 
-ss_status enqueue_history(ss_round *r, const void *k, const void *v, const int32_t *len, long total,
-                          hipStream_t stream) {
+ss_status enqueue_history(ss_round *r, int nchunks, const void *const *k, const void *const *v,
+                          const int32_t *len, const std::vector<long> &tot, hipStream_t stream) {
+  long total = 0;
+  for (long t : tot) total += t;
   if (total == 0) return SS_OK;
   Plan plan;
-  plan_chunk(r, len, total, &plan);
-  ss::ChunkParams *p = base_params(r, k, v, total);
+  ss_status s = plan_chunks(r, nchunks, len, tot, &plan);
+  if (s != SS_OK) return s;
+  ss::ChunkParams *p = base_params(r, nchunks, k, v, tot);
   hipError_t e = launch_items(p, plan.rb2, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 2, stream); });
   if (e == hipSuccess)
     e = launch_items(p, plan.rb1, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 1, stream); });
   if (e == hipSuccess)
     e = launch_items(p, plan.valu, [&](const ss::ChunkParams &q) { return ss::launch_chunk_valu(q, stream); });
   if (e != hipSuccess) return hip_fail(e, "history chunk kernel launch");
-  // slots written by this call are valid from now on
-  for (const auto *lst : {&plan.valu, &plan.rb1, &plan.rb2})
-    for (const ss::Item &it : *lst) {
-      const int b = (int)(std::upper_bound(r->row_off.begin(), r->row_off.end(), it.q_row0) - r->row_off.begin()) - 1;
-      r->slots_used[b] = std::max(r->slots_used[b], (it.slot & 0xff) + 1);
-    }
+  r->slots_used = plan.slots_after;   // the slots written by this call are valid from now on
+  return SS_OK;
+}
+
+ss_status attend_history(ss_round *r, int nchunks, const void *const *k, const void *const *v, const int32_t *len,
+                         hipEvent_t wait_before, hipEvent_t signal_after, hipStream_t stream) {
+  std::vector<long> tot;
+  ss_status s = check_history_args(r, nchunks, k, v, len, &tot);
+  if (s != SS_OK) return s;
+  hipError_t e;
+  if (wait_before != nullptr && (e = hipStreamWaitEvent(stream, wait_before, 0)) != hipSuccess)
+    return hip_fail(e, "hipStreamWaitEvent (history)");
+  s = enqueue_history(r, nchunks, k, v, len, tot, stream);
+  if (s != SS_OK) return s;
+  if (signal_after != nullptr && (e = hipEventRecord(signal_after, stream)) != hipSuccess)
+    return hip_fail(e, "hipEventRecord (history)");
   return SS_OK;
 }
 
@@ -326,19 +373,15 @@ ss_status ss_upload_chunk(void *dst_device, const void *src_pinned_host, size_t 
 
 ss_status ss_attend_history_chunk(ss_round *r, const void *k, const void *v, const int32_t *len,
                                   hipEvent_t wait_before, hipEvent_t signal_after, hipStream_t stream) {
-  long total = 0;
-  ss_status s = check_history_args(r, len, &total);
-  if (s != SS_OK) return s;
-  if (total > 0 && (k == nullptr || v == nullptr || !aligned(k, 16) || !aligned(v, 16)))
-    return fail(SS_ERR_INVALID_ARGUMENT, "k and v must be non-null and 16-byte aligned");
-  hipError_t e;
-  if (wait_before != nullptr && (e = hipStreamWaitEvent(stream, wait_before, 0)) != hipSuccess)
-    return hip_fail(e, "hipStreamWaitEvent (history)");
-  s = enqueue_history(r, k, v, len, total, stream);
-  if (s != SS_OK) return s;
-  if (signal_after != nullptr && (e = hipEventRecord(signal_after, stream)) != hipSuccess)
-    return hip_fail(e, "hipEventRecord (history)");
-  return SS_OK;
+  const void *kk[1] = {k};
+  const void *vv[1] = {v};
+  return attend_history(r, 1, kk, vv, len, wait_before, signal_after, stream);
+}
+
+ss_status ss_attend_history_chunks(ss_round *r, int32_t num_chunks, const void *const *k, const void *const *v,
+                                   const int32_t *len, hipEvent_t wait_before, hipEvent_t signal_after,
+                                   hipStream_t stream) {
+  return attend_history(r, num_chunks, k, v, len, wait_before, signal_after, stream);
 }
 
 ss_status ss_attend_local_candidates(ss_round *r, const void *k_cand, const void *v_cand, hipStream_t stream) {
@@ -423,18 +466,23 @@ ss_status ss_pipeline_create(ss_pipeline **out, void *staging0, void *staging1, 
 ss_status ss_pipeline_attend_chunk(ss_pipeline *p, ss_round *r, const void *host_kv, const int32_t *len,
                                    hipStream_t stream) {
   if (p == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "pipeline is null");
+  std::vector<long> tot;
+  const int sl = p->next;
   long total = 0;
-  ss_status s = check_history_args(r, len, &total);
+  if (len != nullptr && r != nullptr)
+    for (int b = 0; b < r->B; ++b) total += std::max<int32_t>(0, len[b]);
+  const size_t half = r != nullptr ? (size_t)total * r->Hkv * ss::kHeadDim * 2 : 0;
+  const void *kk[1] = {p->slot[sl]};
+  const void *vv[1] = {p->slot[sl] + half};
+  ss_status s = check_history_args(r, 1, kk, vv, len, &tot);
   if (s != SS_OK) return s;
   if (total == 0) return SS_OK;
   if (host_kv == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "host_kv is null");
-  const size_t half = (size_t)total * r->Hkv * ss::kHeadDim * 2;
   if (2 * half > p->slot_bytes)
     return fail(SS_ERR_INVALID_ARGUMENT, "chunk needs %zu bytes > slot_bytes %zu", 2 * half, p->slot_bytes);
-  const int sl = p->next;
   s = ss_upload_chunk(p->slot[sl], host_kv, 2 * half, p->copy, p->used[sl] ? p->freed[sl] : nullptr, p->ready[sl]);
   if (s != SS_OK) return s;
-  s = ss_attend_history_chunk(r, p->slot[sl], p->slot[sl] + half, len, p->ready[sl], p->freed[sl], stream);
+  s = attend_history(r, 1, kk, vv, len, p->ready[sl], p->freed[sl], stream);
   if (s != SS_OK) return s;
   p->used[sl] = true;
   p->next = sl ^ 1;

@@ -7,8 +7,9 @@
 namespace ss {
 
 constexpr int kHeadDim = 128;       // d
-constexpr int kNumSlots = 16;       // split slots of the running state per row
-constexpr int kMaxItems = 200;      // work items per launch (kernel-argument list)
+constexpr int kNumSlots = 32;       // split slots of the running state per row
+constexpr int kMaxItems = 2048;     // work items per launch (kernel-argument list)
+constexpr int kMaxChunks = 32;      // history chunks per launch
 constexpr int kTile = 32;           // history tokens per wave iteration
 constexpr int kWaves = 4;           // waves per workgroup of the chunk kernels
 constexpr int kMaxCand = 8;         // candidates per request (k_b + 1)
@@ -17,20 +18,21 @@ constexpr int kMaxRows = 32;        // rows per KV head the MFMA chunk kernel ha
 
 // Item flag: the slot has not been written in this round yet, so the kernel
 // stores its result instead of merging with (uninitialised) workspace.
-constexpr int kSlotFresh = 0x100;
+constexpr int kSlotFresh = 1;
 
-// History item: one workgroup's share of a chunk for one request (x all KV
-// heads through blockIdx.y): tokens [tok_begin, tok_begin + tok_count) of
-// the packed chunk, folded into split slot (slot & 0xff) of the request's
-// query rows.
+// History item: one workgroup's share of one chunk for one request (x all
+// KV heads through blockIdx.y): tokens [tok_begin, tok_begin + tok_count) of
+// chunk `chunk`, folded into split slot `slot` of the request's query rows.
 // Finalize item: one request; tok_count = number of slots written by
-// history calls (slots >= that are empty), tok_begin unused.
+// history calls (slots >= that are empty), other token fields unused.
 struct Item {
   int32_t tok_begin;
   int32_t tok_count;
   int32_t q_row0;   // off_b: first packed candidate row of the request
-  int16_t n_cand;   // n_b
-  int16_t slot;     // slot index | kSlotFresh
+  uint8_t n_cand;   // n_b
+  uint8_t chunk;    // index into the launch's chunk table
+  uint8_t slot;     // state slot
+  uint8_t flags;    // kSlotFresh
 };
 static_assert(sizeof(Item) == 16, "Item layout");
 
@@ -47,15 +49,16 @@ struct State {
 };
 
 struct ChunkParams {
-  const uint16_t *k;    // bf16 chunk: token-major [sum len][Hkv][d] or head-major [Hkv][sum len][d]
-  const uint16_t *v;
   const uint16_t *q;    // bf16 [sum n_b, Hq, d]
   State st;
   int32_t Hq, Hkv, G;
   float scale_log2;     // softmax_scale * log2(e)
   uint32_t tok_stride;  // elements between consecutive tokens of one KV head
-  uint64_t head_stride; // elements between KV heads at the same token
   int32_t num_items;
+  // chunk table: bf16 chunks, token-major [sum len][Hkv][d] or head-major [Hkv][sum len][d]
+  const uint16_t *k[kMaxChunks];
+  const uint16_t *v[kMaxChunks];
+  uint64_t head_stride[kMaxChunks];   // elements between KV heads at the same token
   Item items[kMaxItems];
 };
 

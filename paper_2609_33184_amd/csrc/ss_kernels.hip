@@ -119,9 +119,9 @@ __device__ __forceinline__ void fold_into_slot(const ChunkParams &p, const Item 
       a[c + 3] += f[w] * x[3];
     }
   }
-  const size_t idx = (size_t)(it.slot & 0xff) * p.st.R + global_row(p, it, g, r);
+  const size_t idx = (size_t)it.slot * p.st.R + global_row(p, it, g, r);
   float *ap = p.st.a + idx * kHeadDim + seg * SEGLEN;
-  if (it.slot & kSlotFresh) {        // first write of this slot in the round: store
+  if (it.flags & kSlotFresh) {       // first write of this slot in the round: store
 #pragma unroll
     for (int c = 0; c < SEGLEN; c += 4)
       *reinterpret_cast<f32x4_t *>(ap + c) = f32x4_t{a[c], a[c + 1], a[c + 2], a[c + 3]};
@@ -230,11 +230,11 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   // Offsets are 32-bit (the host keeps an item below 2^31 bytes).
   const uint32_t stride_b = p.tok_stride * 2;                      // bytes between tokens
   const uint32_t nrec = (uint32_t)(count - 1) * stride_b + kRowBytes;
-  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride;
+  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride[it.chunk];
   const __amdgpu_buffer_rsrc_t krs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k + first), (short)0, (int)nrec, kBufferFlags);
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k[it.chunk] + first), (short)0, (int)nrec, kBufferFlags);
   const __amdgpu_buffer_rsrc_t vrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v + first), (short)0, (int)nrec, kBufferFlags);
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v[it.chunk] + first), (short)0, (int)nrec, kBufferFlags);
   const uint32_t voff = lq * stride_b + 16 * lr;                     // token lq, chunk lr
   unsigned char *qs = smem;
   unsigned char *ks = smem + MfmaLds<RB>::kQBytes + w * (2 * kTileBytes);
@@ -432,11 +432,11 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
   }
   const uint32_t stride_b = p.tok_stride * 2;
   const uint32_t nrec = (uint32_t)(count - 1) * stride_b + 2 * kHeadDim;
-  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride;
+  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride[it.chunk];
   const __amdgpu_buffer_rsrc_t krs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k + first), (short)0, (int)nrec, kBufferFlags);
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k[it.chunk] + first), (short)0, (int)nrec, kBufferFlags);
   const __amdgpu_buffer_rsrc_t vrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v + first), (short)0, (int)nrec, kBufferFlags);
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v[it.chunk] + first), (short)0, (int)nrec, kBufferFlags);
   const uint32_t voff = tg * stride_b + 16 * c;
   const int ntiles = (count + kTile - 1) / kTile;
   const float sl2 = p.scale_log2;
@@ -594,23 +594,15 @@ __global__ void __launch_bounds__(256) finalize_kernel(const FinalParams p) {
     x[j] = j <= i ? x[j] * p.scale_log2 : kNegInf;
     mstar = fmaxf(mstar, x[j]);
   }
-  float ms[kNumSlots];
-#pragma unroll
-  for (int s = 0; s < kNumSlots; ++s) {
-    ms[s] = s < nslot ? p.st.m[(size_t)s * p.st.R + row] : kNegInf;
-    mstar = fmaxf(mstar, ms[s]);
-  }
+  for (int s = 0; s < nslot; ++s) mstar = fmaxf(mstar, p.st.m[(size_t)s * p.st.R + row]);
   float l = 0.f, a0 = 0.f, a1 = 0.f;
-#pragma unroll
-  for (int s = 0; s < kNumSlots; ++s) {
-    if (s < nslot) {
-      const size_t idx = (size_t)s * p.st.R + row;
-      const float f = exp2_fast(ms[s] - mstar);
-      const float2 a = reinterpret_cast<const float2 *>(p.st.a + idx * kHeadDim)[lane];
-      l = fmaf(f, p.st.l[idx], l);
-      a0 = fmaf(f, a.x, a0);
-      a1 = fmaf(f, a.y, a1);
-    }
+  for (int s = 0; s < nslot; ++s) {
+    const size_t idx = (size_t)s * p.st.R + row;
+    const float f = exp2_fast(p.st.m[idx] - mstar);
+    const float2 a = reinterpret_cast<const float2 *>(p.st.a + idx * kHeadDim)[lane];
+    l = fmaf(f, p.st.l[idx], l);
+    a0 = fmaf(f, a.x, a0);
+    a1 = fmaf(f, a.y, a1);
   }
 #pragma unroll
   for (int j = 0; j < kMaxCand; ++j) {

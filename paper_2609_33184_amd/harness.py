@@ -55,13 +55,27 @@ def hbm_history(w: Workload, layer: int = 0, device="cuda", kv_layout: int = ss.
 
 def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor]], stream: int,
               order: Optional[Sequence[int]] = None, cand_position: Optional[int] = None,
-              lens: Optional[Sequence[Sequence[int]]] = None) -> None:
+              lens: Optional[Sequence[Sequence[int]]] = None, batch: int = 1) -> None:
     """Enqueue one whole round (init, history chunks, candidates, finalize)
-    on `stream`; results land in b.out / b.lse."""
+    on `stream`; results land in b.out / b.lse.  ``batch`` > 1 groups that
+    many consecutive chunks into one ss_attend_history_chunks call."""
     w = b.w
     order = list(range(len(chunks))) if order is None else list(order)
     pos = len(order) if cand_position is None else cand_position
     r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream)
+    if batch > 1:
+        try:
+            for i0 in range(0, len(order), batch):
+                grp = order[i0:i0 + batch]
+                ks = [chunks[j][0].data_ptr() if chunks[j][0].numel() else 0 for j in grp]
+                vs = [chunks[j][1].data_ptr() if chunks[j][1].numel() else 0 for j in grp]
+                ls = [w.chunk_lens(j) if lens is None else lens[j] for j in grp]
+                ss.ss_attend_history_chunks(r, ks, vs, ls, None, None, stream)
+            ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
+            ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream)
+        finally:
+            ss.ss_round_destroy(r)
+        return
     try:
         for idx, j in enumerate(order):
             if idx == pos:

@@ -29,6 +29,7 @@ SS_KV_HEAD_MAJOR = 1    # history chunk [Hkv][sum len][d]
 
 EXPORTED = (
     "ss_round_workspace_bytes", "ss_round_init", "ss_upload_chunk", "ss_attend_history_chunk",
+    "ss_attend_history_chunks",
     "ss_attend_local_candidates", "ss_round_finalize", "ss_round_destroy", "ss_pipeline_create",
     "ss_pipeline_attend_chunk", "ss_pipeline_destroy", "ss_event_create", "ss_event_destroy",
     "ss_status_string", "ss_last_error",
@@ -89,6 +90,7 @@ def load() -> ctypes.CDLL:
         "ss_round_init": (I32, [ctypes.POINTER(P), ctypes.POINTER(ss_round_desc), P, P, SZ, P]),
         "ss_upload_chunk": (I32, [P, P, SZ, P, P, P]),
         "ss_attend_history_chunk": (I32, [P, P, P, PI32, P, P, P]),
+        "ss_attend_history_chunks": (I32, [P, I32, ctypes.POINTER(P), ctypes.POINTER(P), PI32, P, P, P]),
         "ss_attend_local_candidates": (I32, [P, P, P, P]),
         "ss_round_finalize": (I32, [P, P, P, P]),
         "ss_round_destroy": (None, [P]),
@@ -149,6 +151,17 @@ def ss_attend_history_chunk(r: int, k: int, v: int, len_: Sequence[int], wait_be
                             signal_after: Optional[int] = None, stream: int = 0) -> None:
     _check(load().ss_attend_history_chunk(r, k, v, _lens(len_), wait_before, signal_after, stream),
            "ss_attend_history_chunk")
+
+
+def ss_attend_history_chunks(r: int, k: Sequence[int], v: Sequence[int], lens: Sequence[Sequence[int]],
+                             wait_before: Optional[int] = None, signal_after: Optional[int] = None,
+                             stream: int = 0) -> None:
+    n = len(k)
+    kp = (ctypes.c_void_p * n)(*k)
+    vp = (ctypes.c_void_p * n)(*v)
+    flat = [int(x) for row in lens for x in row]
+    _check(load().ss_attend_history_chunks(r, n, kp, vp, (ctypes.c_int32 * len(flat))(*flat), wait_before,
+                                           signal_after, stream), "ss_attend_history_chunks")
 
 
 def ss_attend_local_candidates(r: int, k_cand: int, v_cand: int, stream: int = 0) -> None:

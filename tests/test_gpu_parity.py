@@ -92,6 +92,23 @@ def test_config4_sampled_full_size(stream, layout):
     check_sampled(w, b.out, b.lse, pairs, what="config4")
 
 
+@pytest.mark.parametrize("layout", LAYOUTS, ids=LAYOUT_IDS)
+def test_config3_batched_call(stream, layout):
+    """All 8 resident chunks in one ss_attend_history_chunks launch."""
+    w = W.workload(3)
+    print(f"config 3, one batched history call, layout {layout}", flush=True)
+    b = _run(w, stream, kv_layout=layout, batch=8)
+    check_sampled(w, b.out, b.lse, [(1, 2), (8, 5), (14, 0)], what="config3 batched")
+
+
+def test_config4_batched_call(stream):
+    w = W.workload(4)
+    print("config 4, batched history calls (chunks of 4 and 8)", flush=True)
+    for batch in (4, 16):
+        b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR, batch=batch)
+        check_sampled(w, b.out, b.lse, [(0, 1), (5, 6), (63, 3)], what=f"config4 batch={batch}")
+
+
 def test_config5_one_layer_full_size(stream):
     w = W.workload(5)
     print("config 5 (32 x 131072, outliers), one layer in-HBM, head-major", flush=True)
