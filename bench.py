@@ -67,28 +67,36 @@ def time_round_steps(torch, H, b, chunks, stream, steps: int, warmup: int, batch
     return e0.elapsed_time(e1) / 1e3, wall
 
 
-def per_launch_times(torch, ss, b, chunks, stream, rounds: int):
-    """Mean device time of one history-chunk call (one MFMA kernel launch for
-    this workload), from HIP events recorded on the kernel's stream."""
+def per_launch_times(torch, ss, b, chunks, stream, rounds: int, batch: int):
+    """Device time of each history launch of a round (HIP events recorded on
+    the launch's stream around the call; one launch per call here), with the
+    algorithmic KV bytes it attends."""
     w = b.w
     times = []
-    for _ in range(rounds):
+    pending = []
+    for _ in range(rounds + 1):
         evs = []
         r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream.cuda_stream)
-        for j, (k, v) in enumerate(chunks):
+        for i0 in range(0, len(chunks), batch):
+            grp = list(range(i0, min(len(chunks), i0 + batch)))
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-            ss.ss_attend_history_chunk(r, k.data_ptr(), v.data_ptr(), w.chunk_lens(j), None, None,
-                                       stream.cuda_stream)
+            ss.ss_attend_history_chunks(r, [chunks[j][0].data_ptr() for j in grp],
+                                        [chunks[j][1].data_ptr() for j in grp],
+                                        [w.chunk_lens(j) for j in grp], None, None, stream.cuda_stream)
             e1.record(stream)
-            evs.append((e0, e1, j))
+            evs.append((e0, e1, sum(sum(w.chunk_lens(j)) for j in grp) * w.token_bytes()))
         ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream.cuda_stream)
         ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream.cuda_stream)
         ss.ss_round_destroy(r)
-        torch.cuda.synchronize()
-        for e0, e1, j in evs:
-            times.append((e0.elapsed_time(e1) / 1e3, j))
+        pending.append(evs)
+    # rounds are enqueued back to back (the host runs ahead of the GPU, so a
+    # launch's events do not include host-side submission time); read them all
+    torch.cuda.synchronize()
+    for evs in pending[1:] if len(pending) > 1 else pending:
+        for e0, e1, nbytes in evs:
+            times.append((e0.elapsed_time(e1) / 1e3, nbytes))
     return times
 
 
@@ -179,8 +187,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--split-tokens", type=int, default=0)
-    ap.add_argument("--batch", type=int, default=1,
-                    help="history chunks per ss_attend_history_chunks call in the timed round (1 = one call per chunk)")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="history chunks per ss_attend_history_chunks call in the timed round "
+                         "(0 = all resident chunks in one call, 1 = one call per chunk)")
     ap.add_argument("--kv-layout", choices=["token", "head"], default="head",
                     help="history chunk layout: token-major [tok][Hkv][d] or head-major [Hkv][tok][d]")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -222,24 +231,39 @@ def main() -> int:
     stream = torch.cuda.Stream()
     torch.cuda.synchronize()
 
+    batch = w.num_chunks if args.batch == 0 else args.batch
     if args.per_launch_only:
-        times = per_launch_times(torch, ss, b, chunks, stream, max(1, args.steps))
+        times = per_launch_times(torch, ss, b, chunks, stream, max(1, args.steps), batch)
         mean = sum(t for t, _ in times) / len(times)
-        log(f"per-launch mean {mean * 1e6:.1f} us over {len(times)} launches")
+        log(f"per-launch mean {mean * 1e6:.1f} us over {len(times)} launches (batch {batch})")
         return 0
 
-    log("bench: timed rounds")
-    dt, wall = time_round_steps(torch, H, b, chunks, stream, args.steps, args.warmup, args.batch)
+    log(f"bench: timed rounds ({batch} chunk(s) per history call)")
+    dt, wall = time_round_steps(torch, H, b, chunks, stream, args.steps, args.warmup, batch)
     step_s = dt / args.steps
     kv_bytes = w.algorithmic_kv_bytes()
     value = kv_bytes * args.steps / dt / 1e9
 
-    log("bench: per-launch timing of the history-chunk kernel")
-    times = per_launch_times(torch, ss, b, chunks, stream, 5)
-    full = [t for t, j in times if sum(w.chunk_lens(j)) == max(sum(w.chunk_lens(i)) for i in range(w.num_chunks))]
+    log("bench: per-launch timing of the history kernel")
+    times = per_launch_times(torch, ss, b, chunks, stream, 5, batch)
+    big = max(nb for _, nb in times)
+    full = [t for t, nb in times if nb == big]
     launch_s = sum(full) / len(full)
-    bytes_per_launch = max(sum(w.chunk_lens(j)) for j in range(w.num_chunks)) * w.token_bytes()
+    bytes_per_launch = big
     achieved = bytes_per_launch / launch_s / 1e9
+
+    per_chunk = None
+    if batch != 1:
+        log("bench: the same round with one history call per chunk")
+        dt1, _ = time_round_steps(torch, H, b, chunks, stream, args.steps, args.warmup, 1)
+        t1 = per_launch_times(torch, ss, b, chunks, stream, 3, 1)
+        big1 = max(nb for _, nb in t1)
+        l1 = [t for t, nb in t1 if nb == big1]
+        per_chunk = {"round_ms": round(dt1 / args.steps * 1e3, 4),
+                     "effective_KV_GBs": round(kv_bytes * args.steps / dt1 / 1e9, 2),
+                     "pct_of_hbm_peak": round(100.0 * kv_bytes * args.steps / dt1 / 1e9 / HBM_PEAK_GBS, 2),
+                     "mean_launch_us": round(sum(l1) / len(l1) * 1e6, 2),
+                     "launch_GBs": round(big1 / (sum(l1) / len(l1)) / 1e9, 2)}
 
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
@@ -269,12 +293,13 @@ def main() -> int:
                         f"{w.num_chunks} chunks of {w.chunk_tokens}, {w.num_cand[0] if len(set(w.num_cand)) == 1 else 'ragged'} "
                         f"candidate queries, history resident in HBM ({args.kv_layout}-major chunks)",
             "round_latency_ms": round(step_s * 1e3, 4),
+            "chunks_per_history_call": batch,
             "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
             "kv_bytes_per_round": kv_bytes,
             "wall_s_timed": round(wall, 4),
         },
         "roofline": {
-            "kernel": "chunk_attn_mfma<2> (one launch per history chunk)",
+            "kernel": f"chunk_attn_mfma<2> (history launch over {batch} chunk(s))",
             "bound": "hbm",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,
@@ -286,6 +311,8 @@ def main() -> int:
             "launches_timed": len(full),
         },
     }
+    if per_chunk is not None:
+        out["per_chunk_calls"] = per_chunk
     if not args.no_cpu_baseline:
         log("bench: cpu baseline (fp64 oracle on host cores)")
         out["cpu_baseline"] = cpu_baseline(w, chunks, list(range(min(w.B, args.cpu_sample_requests))))

@@ -35,10 +35,12 @@ ss_status hip_fail(hipError_t e, const char *what) {
 inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Workgroups one history chunk aims for (2 resident per CU on 256 CUs).
-constexpr long kTargetWorkgroups = 512;
+// Automatic piece size: large pieces amortise each workgroup's fixed costs
+// (query staging, wave merge, state fold); aim for at least one workgroup per
+// CU (256 on MI355X) per launch and cap a piece at kMaxAutoPiece tokens.
+constexpr long kTargetWorkgroups = 256;
 constexpr int kMinPiece = 256;
-constexpr int kMaxAutoPiece = 2048;
+constexpr int kMaxAutoPiece = 4096;
 constexpr int kDefaultMfmaMinRows = ss::kMaxValuRows + 1;
 
 ss_status validate_desc(const ss_round_desc *d) {
@@ -165,11 +167,8 @@ ss_status plan_chunks(const ss_round *r, int nchunks, const int32_t *len, const 
   if (r->split_tokens > 0) {
     piece = r->split_tokens;
   } else {
-    // ~512 workgroups for one chunk of a large Cohort, never pieces above
-    // kMaxAutoPiece (folds of the running state stay a few % of the KV bytes
-    // while batched launches get enough workgroups to balance the CUs)
-    const long per_chunk_work = (total / nchunks) * r->Hkv;
-    piece = (per_chunk_work + kTargetWorkgroups - 1) / kTargetWorkgroups;
+    const long work = total * r->Hkv;
+    piece = (work + kTargetWorkgroups - 1) / kTargetWorkgroups;
     piece = std::min<long>(kMaxAutoPiece, std::max<long>(kMinPiece, align_up(piece, ss::kTile)));
   }
   const long pmax = max_piece_tokens(r);

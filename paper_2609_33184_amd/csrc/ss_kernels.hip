@@ -243,14 +243,17 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   const float sl2 = p.scale_log2;
 
   u32x4_t kr[8], vr[8];
-  // coalesced loads: instruction i reads tokens tb + 4i + lq, chunk lr
+  // coalesced loads: instruction i reads tokens tb + 4i + lq, chunk lr.  The
+  // whole offset goes in the VGPR operand: the buffer range check covers the
+  // VGPR (and immediate) offset only, not the scalar one, and rows past the
+  // item must come back as zeros rather than read beyond the buffer.
   auto load_kv = [&](int tb) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(krs, voff, (uint32_t)(tb + 4 * i) * stride_b, 0);
+      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(krs, voff + (uint32_t)(tb + 4 * i) * stride_b, 0, 0);
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, voff, (uint32_t)(tb + 4 * i) * stride_b, 0);
+      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, voff + (uint32_t)(tb + 4 * i) * stride_b, 0, 0);
   };
   // K operand read: row 16u + lr, chunk 4s + lq at position (4s + lq) ^ lr
   // V transpose read: row 4lq + lr/4 (+16), chunk 2db + (lr&3)/2, half lr&1
@@ -348,17 +351,24 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
     }
   };
 
-  // first tile in flight before the query rows are staged
-  int t0 = w;
-  if (t0 < ntiles) load_kv(t0 * kTile);
   // Q rows of this (request, kv head) -> LDS, chunk c of row r at c ^ (r & 15);
   // rows >= M are zero.  The Q^T operand (B[k = d][j = row]) of lane (lr, lq),
-  // k-step s, is row lr's d-chunk 4s + lq.
-  for (int c = threadIdx.x; c < RB * 16 * 16; c += 256) {
-    const int r = c >> 4, ch = c & 15;
-    u32x4_t v = {0, 0, 0, 0};
-    if (r < M) v = reinterpret_cast<const u32x4_t *>(p.q + (size_t)global_row(p, it, g, r) * kHeadDim)[ch];
-    *reinterpret_cast<u32x4_t *>(qs + r * kRowBytes + 16 * (ch ^ (r & 15))) = v;
+  // k-step s, is row lr's d-chunk 4s + lq.  The query loads are issued first,
+  // then the first K/V tile, so staging Q waits only for the query rows.
+  constexpr int kQPerThread = RB * 16 * 16 / 256;
+  u32x4_t qv[kQPerThread];
+#pragma unroll
+  for (int e = 0; e < kQPerThread; ++e) {
+    const int c = threadIdx.x + 256 * e, r = c >> 4, ch = c & 15;
+    qv[e] = u32x4_t{0, 0, 0, 0};
+    if (r < M) qv[e] = reinterpret_cast<const u32x4_t *>(p.q + (size_t)global_row(p, it, g, r) * kHeadDim)[ch];
+  }
+  int t0 = w;
+  if (t0 < ntiles) load_kv(t0 * kTile);
+#pragma unroll
+  for (int e = 0; e < kQPerThread; ++e) {
+    const int c = threadIdx.x + 256 * e, r = c >> 4, ch = c & 15;
+    *reinterpret_cast<u32x4_t *>(qs + r * kRowBytes + 16 * (ch ^ (r & 15))) = qv[e];
   }
   __syncthreads();
 
@@ -443,15 +453,16 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
 
   // coalesced loads (4 token rows per instruction); tokens past the item read 0
   u32x4_t kr[8], vr[8];
+  // the whole offset goes in the range-checked VGPR operand (see the MFMA kernel)
   auto load_k = [&](int tb) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(krs, voff, (uint32_t)(tb + 4 * i) * stride_b, 0);
+      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(krs, voff + (uint32_t)(tb + 4 * i) * stride_b, 0, 0);
   };
   auto load_v = [&](int tb) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, voff, (uint32_t)(tb + 4 * i) * stride_b, 0);
+      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, voff + (uint32_t)(tb + 4 * i) * stride_b, 0, 0);
   };
   // one tile per iteration; the next tile's K is issued after the scores, its
   // V after the PV update; the last tile is peeled (unconditional prefetch)

@@ -1,0 +1,226 @@
+"""GPU invariants and pipeline behaviour (through the C ABI).
+
+* Eq. 17: the result does not depend on chunk count, chunk order or where the
+  Speculative Frontier pass sits among the history calls (mutually <= 1e-5);
+* a candidate never sees later candidates: scaling later candidates' K/V by
+  64 leaves earlier rows bitwise unchanged;
+* V x 2 gives O x 2 exactly; V = 1 gives O = 1 (weights sum to 1);
+* streaming the history through the two-slot pipeline gives the in-HBM
+  result bitwise; poisoning a staging slot right after its "free" event or
+  delaying uploads changes nothing;
+* the device generator produces the CPU generator's bits;
+* argument and call-order errors surface as the documented status codes.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_33184_amd import harness as H
+from paper_2609_33184_amd import specstream as ss
+from paper_2609_33184_amd import workloads as W
+from parity import assert_parity, oracle_full
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def stream():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    ss.load()
+    s = torch.cuda.Stream()
+    yield s
+    torch.cuda.synchronize()
+
+
+def _round(w, stream, chunks=None, kv_layout=ss.SS_KV_TOKEN_MAJOR, **kw):
+    b = H.RoundBuffers(w, kv_layout=kv_layout, split_tokens=kw.pop("split_tokens", 0))
+    chunks = H.hbm_history(w, kv_layout=kv_layout) if chunks is None else chunks
+    torch.cuda.synchronize()
+    H.run_round(b, chunks, stream.cuda_stream, **kw)
+    stream.synchronize()
+    return b, chunks
+
+
+def test_generator_device_matches_cpu():
+    w = W.workload(5)
+    print("generator: device vs CPU bits", flush=True)
+    for b in (0, 31):
+        a = w.k_hist(b, 1000, 1100, layer=0, device="cuda").cpu()
+        c = w.k_hist(b, 1000, 1100, layer=0, device="cpu")
+        assert torch.equal(a.view(torch.int16), c.view(torch.int16))
+        assert torch.equal(w.v_cand(b, device="cuda").cpu().view(torch.int16), w.v_cand(b).view(torch.int16))
+        assert torch.equal(w.q(b, layer=7, device="cuda").cpu().view(torch.int16), w.q(b, layer=7).view(torch.int16))
+
+
+def test_chunk_order_and_count_invariance(stream):
+    w = W.custom([3000, 1111, 2048], [5, 2, 8], num_q_heads=32, num_kv_heads=8, chunk_tokens=512, seed_base=11)
+    print("order/count invariance: base round", flush=True)
+    base, chunks = _round(w, stream)
+    ref = base.out.clone()
+    n = w.num_chunks
+    variants = [dict(order=list(reversed(range(n)))),
+                dict(order=list(range(n)), cand_position=0),
+                dict(order=[3, 0, 5, 1, 4, 2] if n == 6 else list(range(n))[::-1], cand_position=2),
+                dict(split_tokens=64),
+                dict(batch=3),
+                dict(batch=n, order=list(reversed(range(n))))]
+    for v in variants:
+        print(f"order/count invariance: {v}", flush=True)
+        b, _ = _round(w, stream, chunks, **v)
+        diff = (b.out - ref).abs().max().item()
+        assert diff <= 1e-5, (v, diff)
+    ref_o, _ = oracle_full(w)
+    assert_parity(ref.double().cpu().numpy(), ref_o, "order base")
+
+
+def test_later_candidates_never_seen(stream):
+    w = W.custom([777, 300], [6, 8], num_q_heads=16, num_kv_heads=4, chunk_tokens=256, seed_base=12)
+    b, chunks = _round(w, stream)
+    ref = b.out.clone()
+    offs = w.row_offsets()
+    for j in range(1, 6):
+        print(f"mask invariance: candidates >= {j} scaled x64", flush=True)
+        b2 = H.RoundBuffers(w)
+        for bb in range(w.B):
+            sl = slice(offs[bb] + j, offs[bb] + w.num_cand[bb])
+            b2.kc[sl] *= 64
+            b2.vc[sl] *= 64
+        torch.cuda.synchronize()
+        H.run_round(b2, chunks, stream.cuda_stream)
+        stream.synchronize()
+        for bb in range(w.B):
+            early = slice(offs[bb], offs[bb] + j)
+            assert torch.equal(b2.out[early], ref[early]), (bb, j)
+            late = slice(offs[bb] + j, offs[bb] + w.num_cand[bb])
+            assert not torch.equal(b2.out[late], ref[late])
+
+
+def test_value_scaling_and_weights(stream):
+    w = W.custom([2000, 64], [4, 1], num_q_heads=32, num_kv_heads=8, chunk_tokens=1024, seed_base=13)
+    b, chunks = _round(w, stream)
+    ref = b.out.clone()
+    print("V x 2 -> O x 2 bitwise", flush=True)
+    chunks2 = [(k, v * 2) for k, v in chunks]
+    b2 = H.RoundBuffers(w)
+    b2.vc.mul_(2)
+    torch.cuda.synchronize()
+    H.run_round(b2, chunks2, stream.cuda_stream)
+    stream.synchronize()
+    assert torch.equal(b2.out, ref * 2)
+    print("V = 1 -> O = 1", flush=True)
+    chunks1 = [(k, torch.ones_like(v)) for k, v in chunks]
+    b3 = H.RoundBuffers(w)
+    b3.vc.fill_(1)
+    torch.cuda.synchronize()
+    H.run_round(b3, chunks1, stream.cuda_stream)
+    stream.synchronize()
+    assert (b3.out - 1).abs().max().item() <= 1e-5
+
+
+@pytest.mark.parametrize("layout", [ss.SS_KV_TOKEN_MAJOR, ss.SS_KV_HEAD_MAJOR], ids=["token_major", "head_major"])
+def test_streamed_equals_in_hbm(stream, layout):
+    for w in (W.workload(1), W.custom([5000, 123, 4096], [3, 8, 1], num_q_heads=32, num_kv_heads=8,
+                                      chunk_tokens=1024, seed_base=14)):
+        print(f"streamed vs in-HBM: {w.name} layout {layout}", flush=True)
+        b, _ = _round(w, stream, kv_layout=layout)
+        ref = b.out.clone()
+        host = H.HostHistory(w, kv_layout=layout)
+        pipe = H.Pipeline(host.max_chunk_bytes())
+        try:
+            b2 = H.RoundBuffers(w, kv_layout=layout)
+            torch.cuda.synchronize()
+            H.run_round_streamed(b2, host, pipe, stream.cuda_stream)
+            stream.synchronize()
+            assert torch.equal(b2.out, ref)
+        finally:
+            pipe.close()
+
+
+def test_pipeline_poison_and_delay(stream):
+    """A staging slot overwritten with NaNs right after its free event, and
+    uploads delayed behind long copy-stream work, change nothing."""
+    w = W.custom([6000, 2500], [5, 4], num_q_heads=32, num_kv_heads=8, chunk_tokens=1024, seed_base=15)
+    b, _ = _round(w, stream)
+    ref = b.out.clone()
+    host = H.HostHistory(w)
+    nbytes = host.max_chunk_bytes()
+    slots = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    poison = torch.full((nbytes,), 0xFF, dtype=torch.uint8).pin_memory()   # bf16 0xFFFF is NaN
+    copy = torch.cuda.Stream()
+    ready = [ss.ss_event_create() for _ in range(2)]
+    free = [ss.ss_event_create() for _ in range(2)]
+    busy = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+    try:
+        for delay in (False, True):
+            print(f"pipeline poison, delay={delay}", flush=True)
+            b2 = H.RoundBuffers(w)
+            torch.cuda.synchronize()
+            r = ss.ss_round_init(b2.desc, b2.q.data_ptr(), b2.ws.data_ptr(), b2.ws_bytes, stream.cuda_stream)
+            try:
+                for j in range(w.num_chunks):
+                    s = j % 2
+                    lens = w.chunk_lens(j)
+                    half = sum(lens) * w.token_bytes() // 2
+                    if delay:
+                        with torch.cuda.stream(copy):
+                            for _ in range(4):
+                                busy.add_(1)
+                    ss.ss_upload_chunk(slots[s].data_ptr(), host.chunk_ptr(j), 2 * half, copy.cuda_stream,
+                                       free[s] if j >= 2 else None, ready[s])
+                    ss.ss_attend_history_chunk(r, slots[s].data_ptr(), slots[s].data_ptr() + half, lens,
+                                               ready[s], free[s], stream.cuda_stream)
+                    # overwrite the slot as soon as the library says it is free
+                    ss.ss_upload_chunk(slots[s].data_ptr(), poison.data_ptr(), 2 * half, copy.cuda_stream,
+                                       free[s], None)
+                ss.ss_attend_local_candidates(r, b2.kc.data_ptr(), b2.vc.data_ptr(), stream.cuda_stream)
+                ss.ss_round_finalize(r, b2.out.data_ptr(), b2.lse.data_ptr(), stream.cuda_stream)
+            finally:
+                ss.ss_round_destroy(r)
+            torch.cuda.synchronize()
+            assert torch.equal(b2.out, ref)
+    finally:
+        for e in ready + free:
+            ss.ss_event_destroy(e)
+
+
+def test_abi_errors_on_gpu(stream):
+    w = W.workload(1)
+    b = H.RoundBuffers(w)
+    chunks = H.hbm_history(w)
+    k, v = chunks[0]
+    s = stream.cuda_stream
+    # unpinned upload source
+    pageable = torch.zeros(1024, dtype=torch.uint8)
+    with pytest.raises(ss.SpecStreamError) as e:
+        ss.ss_upload_chunk(k.data_ptr(), pageable.data_ptr(), 1024, s)
+    assert e.value.status == ss.SS_ERR_NOT_PINNED
+    # call order
+    r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, s)
+    try:
+        with pytest.raises(ss.SpecStreamError) as e:
+            ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), s)
+        assert e.value.status == ss.SS_ERR_BAD_STATE
+        ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), s)
+        with pytest.raises(ss.SpecStreamError) as e:
+            ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), s)
+        assert e.value.status == ss.SS_ERR_BAD_STATE
+        with pytest.raises(ss.SpecStreamError) as e:                 # too many tokens
+            ss.ss_attend_history_chunk(r, k.data_ptr(), v.data_ptr(), [1 << 20], None, None, s)
+        assert e.value.status == ss.SS_ERR_INVALID_ARGUMENT
+        with pytest.raises(ss.SpecStreamError) as e:                 # misaligned chunk pointer
+            ss.ss_attend_history_chunk(r, k.data_ptr() + 2, v.data_ptr(), [1024], None, None, s)
+        assert e.value.status == ss.SS_ERR_INVALID_ARGUMENT
+        ss.ss_attend_history_chunk(r, k.data_ptr(), v.data_ptr(), [1024], None, None, s)
+        ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), s)
+        with pytest.raises(ss.SpecStreamError) as e:
+            ss.ss_attend_history_chunk(r, k.data_ptr(), v.data_ptr(), [1024], None, None, s)
+        assert e.value.status == ss.SS_ERR_BAD_STATE
+    finally:
+        ss.ss_round_destroy(r)
+    torch.cuda.synchronize()
+    # workspace too small
+    with pytest.raises(ss.SpecStreamError) as e:
+        ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes - 256, s)
+    assert e.value.status == ss.SS_ERR_WORKSPACE
