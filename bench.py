@@ -144,15 +144,20 @@ def cpu_baseline(w, chunks, sample_requests):
                       f"same seeded inputs; GB/s of KV processed"}
 
 
-def streamed_round(torch, H, w, b, stream, rounds: int):
+def streamed_round(torch, H, w, b, chunks, stream, rounds: int):
+    """The round with its history streamed from pinned host memory through the
+    two-slot pipeline (one call per chunk); its output is compared bitwise with
+    the same per-chunk round over the resident chunks."""
     log("streamed: filling pinned host history")
+    H.run_round(b, chunks, stream.cuda_stream, batch=1)
+    torch.cuda.synchronize()
+    ref = b.out.clone()
     host = H.HostHistory(w, kv_layout=b.kv_layout)
     pipe = H.Pipeline(host.max_chunk_bytes())
     try:
         for _ in range(2):
             H.run_round_streamed(b, host, pipe, stream.cuda_stream)
         torch.cuda.synchronize()
-        ref = b.out.clone()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
@@ -317,7 +322,7 @@ def main() -> int:
         log("bench: cpu baseline (fp64 oracle on host cores)")
         out["cpu_baseline"] = cpu_baseline(w, chunks, list(range(min(w.B, args.cpu_sample_requests))))
     if not args.no_streamed:
-        t_stream, t_h2d, h2d_bytes, same = streamed_round(torch, H, w, b, stream, 3)
+        t_stream, t_h2d, h2d_bytes, same = streamed_round(torch, H, w, b, chunks, stream, 3)
         out["streamed"] = {
             "round_ms": round(t_stream * 1e3, 3),
             "h2d_only_ms": round(t_h2d * 1e3, 3),

@@ -20,7 +20,7 @@ import torch
 from paper_2609_33184_amd import harness as H
 from paper_2609_33184_amd import specstream as ss
 from paper_2609_33184_amd import workloads as W
-from parity import assert_parity, oracle_full
+from parity import assert_parity, check_sampled, oracle_full
 
 pytestmark = pytest.mark.gpu
 
@@ -224,3 +224,27 @@ def test_abi_errors_on_gpu(stream):
     with pytest.raises(ss.SpecStreamError) as e:
         ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes - 256, s)
     assert e.value.status == ss.SS_ERR_WORKSPACE
+
+
+def test_config5_streamed_layers(stream):
+    """Config 5: the 16 GiB history streamed from pinned host memory through
+    one continuous two-slot pipeline for several layers in a row (each layer
+    its own queries), sampled parity per layer."""
+    w = W.workload(5)
+    layout = ss.SS_KV_HEAD_MAJOR
+    layers = (0, 35)
+    print("config 5 streamed: filling 16 GiB of pinned host history", flush=True)
+    host = H.HostHistory(w, kv_layout=layout)
+    pipe = H.Pipeline(host.max_chunk_bytes())
+    try:
+        bufs = [H.RoundBuffers(w, layer=l, kv_layout=layout) for l in layers]
+        torch.cuda.synchronize()
+        for l, b in zip(layers, bufs):
+            print(f"config 5 streamed: layer {l}", flush=True)
+            H.run_round_streamed(b, host, pipe, stream.cuda_stream)
+        stream.synchronize()
+    finally:
+        pipe.close()
+    del host
+    for l, b in zip(layers, bufs):
+        check_sampled(w, b.out, b.lse, [(3, 2), (30, 7)], layer=l, what=f"config5 streamed layer {l}")
