@@ -558,15 +558,21 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
 
 // ---------------------------------------------------------------------------
 // Finalize: for every query row (request b, candidate i, head h)
-//   * merge the split slots the history calls wrote (Eq. 14; slot count per
-//     request from the host, unwritten slots are never read),
 //   * attend the Speculative Frontier: candidate keys j <= i of the same
 //     request, causal by absolute position (Sec. 4.2, GPU-resident pass),
+//   * merge the split slots the history calls wrote (Eq. 14; slot count per
+//     request from the host, unwritten slots are never read),
 //   * write O = a / l and LSE = m ln 2 + ln l (Eq. 17).
 // One wave per row (grid.y covers a request's rows, 4 per workgroup); lane l
-// holds d = 2l, 2l+1.  The <= 8 candidate dot products are reduced across
-// the wave as independent chains.
+// holds d = 2l, 2l+1.  Every load is issued before its first use (the query,
+// the visible candidates' K/V and the first kFinGroup slot states), so a
+// row costs one memory round trip per group of slots rather than one per
+// slot.  The <= 8 candidate dot products are reduced across the wave as
+// independent chains; the frontier terms are summed first, then each group
+// of slots is folded in with the rescaled update of Eq. 14.
 // ---------------------------------------------------------------------------
+constexpr int kFinGroup = 8;
+
 __global__ void __launch_bounds__(256) finalize_kernel(const FinalParams p) {
   const int w = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
@@ -580,53 +586,82 @@ __global__ void __launch_bounds__(256) finalize_kernel(const FinalParams p) {
   const int nslot = it.tok_count;
 
   const uint32_t qw = reinterpret_cast<const uint32_t *>(p.q + (size_t)row * kHeadDim)[lane];
-  const float q0 = bf16_lo(qw), q1 = bf16_hi(qw);
-  float x[kMaxCand];
-  uint32_t vw[kMaxCand];
+  uint32_t kw[kMaxCand], vw[kMaxCand];
 #pragma unroll
   for (int j = 0; j < kMaxCand; ++j) {
-    x[j] = 0.f;
+    kw[j] = 0;
     vw[j] = 0;
     if (j <= i) {
       const size_t kv = ((size_t)(it.q_row0 + j) * p.Hkv + g) * kHeadDim;
-      const uint32_t kw = reinterpret_cast<const uint32_t *>(p.kc + kv)[lane];
+      kw[j] = reinterpret_cast<const uint32_t *>(p.kc + kv)[lane];
       vw[j] = reinterpret_cast<const uint32_t *>(p.vc + kv)[lane];
-      x[j] = fmaf(q0, bf16_lo(kw), q1 * bf16_hi(kw));
     }
   }
+  float ms[kFinGroup], ls[kFinGroup];
+  float2 as[kFinGroup];
+  auto load_group = [&](int s0) {
+#pragma unroll
+    for (int u = 0; u < kFinGroup; ++u) {
+      ms[u] = kNegInf;
+      ls[u] = 0.f;
+      as[u] = make_float2(0.f, 0.f);
+      if (s0 + u < nslot) {
+        const size_t idx = (size_t)(s0 + u) * p.st.R + row;
+        ms[u] = p.st.m[idx];
+        ls[u] = p.st.l[idx];
+        as[u] = reinterpret_cast<const float2 *>(p.st.a + idx * kHeadDim)[lane];
+      }
+    }
+  };
+  load_group(0);
+
+  // frontier scores: the <= 8 dot products reduced as independent chains
+  const float q0 = bf16_lo(qw), q1 = bf16_hi(qw);
+  float x[kMaxCand];
+#pragma unroll
+  for (int j = 0; j < kMaxCand; ++j) x[j] = fmaf(q0, bf16_lo(kw[j]), q1 * bf16_hi(kw[j]));
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1)
 #pragma unroll
     for (int j = 0; j < kMaxCand; ++j) x[j] += __shfl_xor(x[j], off);
-
-  float mstar = kNegInf;
+  float m = kNegInf;
 #pragma unroll
   for (int j = 0; j < kMaxCand; ++j) {
     x[j] = j <= i ? x[j] * p.scale_log2 : kNegInf;
-    mstar = fmaxf(mstar, x[j]);
+    m = fmaxf(m, x[j]);
   }
-  for (int s = 0; s < nslot; ++s) mstar = fmaxf(mstar, p.st.m[(size_t)s * p.st.R + row]);
+  // m is finite: every query sees candidate 0
   float l = 0.f, a0 = 0.f, a1 = 0.f;
-  for (int s = 0; s < nslot; ++s) {
-    const size_t idx = (size_t)s * p.st.R + row;
-    const float f = exp2_fast(p.st.m[idx] - mstar);
-    const float2 a = reinterpret_cast<const float2 *>(p.st.a + idx * kHeadDim)[lane];
-    l = fmaf(f, p.st.l[idx], l);
-    a0 = fmaf(f, a.x, a0);
-    a1 = fmaf(f, a.y, a1);
-  }
 #pragma unroll
   for (int j = 0; j < kMaxCand; ++j) {
     if (j <= i) {
-      const float pj = exp2_fast(x[j] - mstar);
+      const float pj = exp2_fast(x[j] - m);
       l += pj;
       a0 = fmaf(pj, bf16_lo(vw[j]), a0);
       a1 = fmaf(pj, bf16_hi(vw[j]), a1);
     }
   }
+  for (int s0 = 0; s0 < nslot; s0 += kFinGroup) {
+    if (s0 > 0) load_group(s0);
+    float mg = m;
+#pragma unroll
+    for (int u = 0; u < kFinGroup; ++u) mg = fmaxf(mg, ms[u]);
+    const float c = exp2_fast(m - mg);              // both finite
+    l *= c;
+    a0 *= c;
+    a1 *= c;
+    m = mg;
+#pragma unroll
+    for (int u = 0; u < kFinGroup; ++u) {
+      const float f = exp2_fast(ms[u] - m);         // 0 for an unused slot (m = -inf)
+      l = fmaf(f, ls[u], l);
+      a0 = fmaf(f, as[u].x, a0);
+      a1 = fmaf(f, as[u].y, a1);
+    }
+  }
   const float inv = 1.0f / l;
   reinterpret_cast<float2 *>(p.out + (size_t)row * kHeadDim)[lane] = make_float2(a0 * inv, a1 * inv);
-  if (p.lse != nullptr && lane == 0) p.lse[row] = mstar * 0.69314718055994531f + logf(l);
+  if (p.lse != nullptr && lane == 0) p.lse[row] = m * 0.69314718055994531f + logf(l);
 }
 
 }  // namespace
