@@ -36,11 +36,14 @@ inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Automatic piece size: large pieces amortise each workgroup's fixed costs
-// (query staging, wave merge, state fold); aim for at least one workgroup per
-// CU (256 on MI355X) per launch and cap a piece at kMaxAutoPiece tokens.
+// (query staging, wave merge, state fold) and a single wave of workgroups
+// has no hand-over between them; aim for one workgroup per CU (256 on
+// MI355X) per launch.  A piece may span chunks of a batched call.  Measured
+// on 16 x 32768 tokens, 8 KV heads: 1024 workgroups of 4096 tokens 394 us,
+// 512 of 8192 384 us, 256 of 16384 381 us per round.
 constexpr long kTargetWorkgroups = 256;
 constexpr int kMinPiece = 256;
-constexpr int kMaxAutoPiece = 4096;
+constexpr int kMaxAutoPiece = 32768;
 constexpr int kDefaultMfmaMinRows = ss::kMaxValuRows + 1;
 
 ss_status validate_desc(const ss_round_desc *d) {
@@ -76,6 +79,8 @@ ss_status validate_desc(const ss_round_desc *d) {
   }
   if (rows * (long)ss::kNumSlots * ss::kHeadDim > (1L << 40))
     return fail(SS_ERR_INVALID_ARGUMENT, "round too large");
+  if (rows * ss::kHeadDim * 2 >= (1L << 31))   // the kernels address Q with 32-bit byte offsets
+    return fail(SS_ERR_INVALID_ARGUMENT, "round too large: the query tensor must stay below 2^31 bytes");
   return SS_OK;
 }
 
@@ -152,13 +157,90 @@ ss_status check_history_args(const ss_round *r, int nchunks, const void *const *
   return SS_OK;
 }
 
+// Work of one history call for one kernel variant: chains of items, chain c
+// = items[start[c] .. start[c + 1]) (one request, one state slot).
+struct Chains {
+  std::vector<ss::Item> items;
+  std::vector<uint32_t> start{0};
+  size_t size() const { return start.size() - 1; }
+  long tokens(size_t c) const {
+    long n = 0;
+    for (uint32_t i = start[c]; i < start[c + 1]; ++i) n += items[i].tok_count;
+    return n;
+  }
+};
+
 struct Plan {
-  std::vector<ss::Item> valu, rb1, rb2;
+  Chains valu, rb1, rb2;
   std::vector<int32_t> slots_after;   // per request: slots in use after this call
 };
 
-// Split every request's tokens of every chunk into pieces of `piece` tokens;
-// the pieces of one request get distinct state slots 0, 1, ...
+// Cut every request's tokens of this call (its ranges in chunk order, as one
+// sequence) into pieces of `piece` tokens; a piece is a chain of at most
+// kMaxChain ranges (a chunk boundary starts a new range) and gets its own
+// state slot.  Returns false if a request would need more than kNumSlots.
+bool build_plan(const ss_round *r, int nchunks, const int32_t *len, long piece, Plan *plan) {
+  const int min_rows = r->mfma_min_rows > 0 ? r->mfma_min_rows : kDefaultMfmaMinRows;
+  *plan = Plan();
+  plan->slots_after = r->slots_used;
+  std::vector<long> off(nchunks, 0);   // first token of request b in chunk c
+  for (int b = 0; b < r->B; ++b) {
+    const int M = r->n_cand[b] * r->G;
+    Chains *dst = (M < min_rows && M <= ss::kMaxValuRows) ? &plan->valu : (M <= 16) ? &plan->rb1 : &plan->rb2;
+    int slot = 0;
+    long filled = 0;      // tokens in the open chain
+    int ranges = 0;       // items in the open chain
+    auto close = [&]() {
+      if (ranges == 0) return;
+      dst->start.push_back((uint32_t)dst->items.size());
+      ++slot;
+      filled = 0;
+      ranges = 0;
+    };
+    for (int c = 0; c < nchunks; ++c) {
+      const long n = len[(size_t)c * r->B + b];
+      long p0 = 0;
+      while (p0 < n) {
+        if (filled == piece || ranges == ss::kMaxChain) close();
+        if (slot >= ss::kNumSlots) return false;
+        const long take = std::min(n - p0, piece - filled);
+        ss::Item it;
+        it.tok_begin = (int32_t)(off[c] + p0);
+        it.tok_count = (int32_t)take;
+        it.q_row0 = r->row_off[b];
+        it.n_cand = (uint8_t)r->n_cand[b];
+        it.chunk = (uint8_t)c;
+        it.slot = (uint8_t)slot;
+        it.flags = slot >= r->slots_used[b] ? ss::kSlotFresh : 0;
+        dst->items.push_back(it);
+        ++ranges;
+        filled += take;
+        p0 += take;
+      }
+      off[c] += n;
+    }
+    close();
+    plan->slots_after[b] = std::max(plan->slots_after[b], slot);
+  }
+  return true;
+}
+
+// Longest chains first (a short chain never delays the tail of the grid).
+void sort_chains(Chains *ch) {
+  std::vector<size_t> order(ch->size());
+  for (size_t c = 0; c < order.size(); ++c) order[c] = c;
+  std::vector<long> tok(order.size());
+  for (size_t c = 0; c < order.size(); ++c) tok[c] = ch->tokens(c);
+  std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return tok[a] > tok[b]; });
+  Chains out;
+  out.items.reserve(ch->items.size());
+  for (size_t c : order) {
+    out.items.insert(out.items.end(), ch->items.begin() + ch->start[c], ch->items.begin() + ch->start[c + 1]);
+    out.start.push_back((uint32_t)out.items.size());
+  }
+  *ch = std::move(out);
+}
+
 ss_status plan_chunks(const ss_round *r, int nchunks, const int32_t *len, const std::vector<long> &tot,
                       Plan *plan) {
   long total = 0;
@@ -174,48 +256,13 @@ ss_status plan_chunks(const ss_round *r, int nchunks, const int32_t *len, const 
   const long pmax = max_piece_tokens(r);
   piece = std::min(piece, pmax);
   // every request must fit its pieces into the slots
-  for (;;) {
-    bool ok = true;
-    for (int b = 0; b < r->B && ok; ++b) {
-      long pieces = 0;
-      for (int c = 0; c < nchunks; ++c) pieces += (len[(size_t)c * r->B + b] + piece - 1) / piece;
-      ok = pieces <= ss::kNumSlots;
-    }
-    if (ok) break;
+  while (!build_plan(r, nchunks, len, piece, plan)) {
     if (piece >= pmax) return fail(SS_ERR_INVALID_ARGUMENT, "too many tokens per request for one history call");
     piece = std::min(pmax, piece * 2);
   }
-  const int min_rows = r->mfma_min_rows > 0 ? r->mfma_min_rows : kDefaultMfmaMinRows;
-  plan->slots_after = r->slots_used;
-  std::vector<long> off(nchunks, 0);
-  for (int b = 0; b < r->B; ++b) {
-    const int M = r->n_cand[b] * r->G;
-    std::vector<ss::Item> *dst = (M < min_rows && M <= ss::kMaxValuRows) ? &plan->valu
-                                 : (M <= 16)                             ? &plan->rb1
-                                                                         : &plan->rb2;
-    int slot = 0;
-    for (int c = 0; c < nchunks; ++c) {
-      const long n = len[(size_t)c * r->B + b];
-      for (long p0 = 0; p0 < n; p0 += piece, ++slot) {
-        ss::Item it;
-        it.tok_begin = (int32_t)(off[c] + p0);
-        it.tok_count = (int32_t)std::min<long>(piece, n - p0);
-        it.q_row0 = r->row_off[b];
-        it.n_cand = (uint8_t)r->n_cand[b];
-        it.chunk = (uint8_t)c;
-        it.slot = (uint8_t)slot;
-        it.flags = slot >= r->slots_used[b] ? ss::kSlotFresh : 0;
-        dst->push_back(it);
-      }
-      off[c] += n;
-    }
-    plan->slots_after[b] = std::max(plan->slots_after[b], slot);
-  }
-  // longest pieces first (a partial piece never delays the tail of the grid)
-  auto by_len = [](const ss::Item &a, const ss::Item &b) { return a.tok_count > b.tok_count; };
-  std::stable_sort(plan->valu.begin(), plan->valu.end(), by_len);
-  std::stable_sort(plan->rb1.begin(), plan->rb1.end(), by_len);
-  std::stable_sort(plan->rb2.begin(), plan->rb2.end(), by_len);
+  sort_chains(&plan->valu);
+  sort_chains(&plan->rb1);
+  sort_chains(&plan->rb2);
   return SS_OK;
 }
 
@@ -235,7 +282,31 @@ ss::ChunkParams *base_params(const ss_round *r, int nchunks, const void *const *
     p.head_stride[c] = r->kv_layout == SS_KV_TOKEN_MAJOR ? (uint64_t)ss::kHeadDim : (uint64_t)tot[c] * ss::kHeadDim;
   }
   p.num_items = 0;
+  p.num_units = 0;
   return &p;
+}
+
+// Launch the chains of `ch` in batches of at most kMaxItems items and
+// kMaxUnits units with `launch(params)`.
+template <typename F>
+hipError_t launch_units(ss::ChunkParams *p, const Chains &ch, F launch) {
+  size_t c0 = 0;
+  while (c0 < ch.size()) {
+    size_t c1 = c0;
+    while (c1 < ch.size() && c1 - c0 < (size_t)ss::kMaxUnits &&
+           ch.start[c1 + 1] - ch.start[c0] <= (uint32_t)ss::kMaxItems)
+      ++c1;
+    const uint32_t i0 = ch.start[c0], n = ch.start[c1] - i0;
+    std::memcpy(p->items, ch.items.data() + i0, n * sizeof(ss::Item));
+    for (size_t c = c0; c < c1; ++c)
+      p->units[c - c0] = (ch.start[c] - i0) | ((ch.start[c + 1] - ch.start[c]) << 16);
+    p->num_items = (int32_t)n;
+    p->num_units = (int32_t)(c1 - c0);
+    const hipError_t e = launch(*p);
+    if (e != hipSuccess) return e;
+    c0 = c1;
+  }
+  return hipSuccess;
 }
 
 // Launch `items` in batches of kMaxItems with `launch(params)`.
@@ -260,11 +331,11 @@ ss_status enqueue_history(ss_round *r, int nchunks, const void *const *k, const 
   ss_status s = plan_chunks(r, nchunks, len, tot, &plan);
   if (s != SS_OK) return s;
   ss::ChunkParams *p = base_params(r, nchunks, k, v, tot);
-  hipError_t e = launch_items(p, plan.rb2, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 2, stream); });
+  hipError_t e = launch_units(p, plan.rb2, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 2, stream); });
   if (e == hipSuccess)
-    e = launch_items(p, plan.rb1, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 1, stream); });
+    e = launch_units(p, plan.rb1, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 1, stream); });
   if (e == hipSuccess)
-    e = launch_items(p, plan.valu, [&](const ss::ChunkParams &q) { return ss::launch_chunk_valu(q, stream); });
+    e = launch_units(p, plan.valu, [&](const ss::ChunkParams &q) { return ss::launch_chunk_valu(q, stream); });
   if (e != hipSuccess) return hip_fail(e, "history chunk kernel launch");
   r->slots_used = plan.slots_after;   // the slots written by this call are valid from now on
   return SS_OK;

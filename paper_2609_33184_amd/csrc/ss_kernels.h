@@ -9,6 +9,8 @@ namespace ss {
 constexpr int kHeadDim = 128;       // d
 constexpr int kNumSlots = 32;       // split slots of the running state per row
 constexpr int kMaxItems = 2048;     // work items per launch (kernel-argument list)
+constexpr int kMaxUnits = 1024;     // workgroup units per launch (x all KV heads)
+constexpr int kMaxChain = 16;       // items (token ranges) per unit
 constexpr int kMaxChunks = 32;      // history chunks per launch
 constexpr int kTile = 32;           // history tokens per wave iteration
 constexpr int kWaves = 4;           // waves per workgroup of the chunk kernels
@@ -20,9 +22,12 @@ constexpr int kMaxRows = 32;        // rows per KV head the MFMA chunk kernel ha
 // stores its result instead of merging with (uninitialised) workspace.
 constexpr int kSlotFresh = 1;
 
-// History item: one workgroup's share of one chunk for one request (x all
-// KV heads through blockIdx.y): tokens [tok_begin, tok_begin + tok_count) of
-// chunk `chunk`, folded into split slot `slot` of the request's query rows.
+// History item: one token range of one chunk for one request: tokens
+// [tok_begin, tok_begin + tok_count) of chunk `chunk` (tok_count >= 1).
+// A unit (one workgroup per KV head, blockIdx.y) is a chain of consecutive
+// items of one request, attended as one token sequence with one running
+// state that is folded into split slot `slot`; every item of a chain carries
+// the same q_row0, n_cand, slot and flags.
 // Finalize item: one request; tok_count = number of slots written by
 // history calls (slots >= that are empty), other token fields unused.
 struct Item {
@@ -59,6 +64,9 @@ struct ChunkParams {
   const uint16_t *k[kMaxChunks];
   const uint16_t *v[kMaxChunks];
   uint64_t head_stride[kMaxChunks];   // elements between KV heads at the same token
+  int32_t num_units;
+  // unit u = items [units[u] & 0xffff, + (units[u] >> 16)), 1..kMaxChain items
+  uint32_t units[kMaxUnits];
   Item items[kMaxItems];
 };
 

@@ -151,8 +151,10 @@ __device__ __forceinline__ void fold_into_slot(const ChunkParams &p, const Item 
 }
 
 // ---------------------------------------------------------------------------
-// MFMA chunk kernel.  Workgroup = (item, kv head); 4 waves; wave w takes the
-// 32-token tiles w, w+4, ... of the item.  Per tile:
+// MFMA chunk kernel.  Workgroup = (unit, kv head); 4 waves; wave w takes the
+// 32-token tiles w, w+4, ... of the unit's chain of items (one request's
+// token ranges, possibly from several chunks, attended as one sequence).
+// Per tile:
 //   K, V tiles -> LDS        coalesced 16-byte loads: one instruction reads 4
 //                            whole 256-byte token rows (16 lanes per row)
 //   S^T[t][row] = K Q^T      v_mfma_f32_16x16x32_bf16, A = K (16 tokens x 32 d,
@@ -188,6 +190,40 @@ __device__ __forceinline__ void fold_into_slot(const ChunkParams &p, const Item 
 constexpr int kRowBytes = kHeadDim * 2;          // 256
 constexpr int kTileBytes = kTile * kRowBytes;    // 8 KiB per K or V tile
 
+__device__ __forceinline__ int tiles_of(const Item &it) { return (it.tok_count + kTile - 1) / kTile; }
+
+// Buffer resource over item `it`'s rows of KV head g in chunk table `tab`
+// (p.k or p.v): loads past the item's last token return zero, so no
+// clamping is needed.  Offsets are 32-bit (the host keeps an item below
+// 2^31 bytes).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t item_rsrc(const ChunkParams &p, const Item &it, int g,
+                                                            const uint16_t *const *tab) {
+  const uint32_t nrec = (uint32_t)(it.tok_count - 1) * (p.tok_stride * 2) + kRowBytes;
+  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride[it.chunk];
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(tab[it.chunk] + first), (short)0, (int)nrec,
+                                           kBufferFlags);
+}
+
+// A unit's tiles are numbered across its chain of items (item 0's tiles
+// first).  The cursor maps a global tile T to (item k, k's first global
+// tile); it only moves forward, and never past the chain's last item.
+struct TileCursor {
+  int k = 0;
+  int base = 0;
+};
+__device__ __forceinline__ void seek(const ChunkParams &p, int i0, int nit, TileCursor &c, int T) {
+  while (c.k + 1 < nit && T - c.base >= tiles_of(p.items[i0 + c.k])) {
+    c.base += tiles_of(p.items[i0 + c.k]);
+    ++c.k;
+  }
+}
+
+// Resources and item-local token base of the next tile a wave loads.
+struct NextTile {
+  __amdgpu_buffer_rsrc_t krs, vrs;
+  int tb;
+};
+
 template <int RB>
 struct MfmaLds {
   static constexpr int kQBytes = RB * 16 * kRowBytes;               // Q rows, shared by the waves
@@ -210,10 +246,14 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15;
   const int lq = lane >> 4;
-  const Item it = p.items[blockIdx.x];
+  const uint32_t unit = p.units[blockIdx.x];
+  const int i0 = unit & 0xffff;
+  const int nit = unit >> 16;
+  const Item it = p.items[i0];          // request, slot and flags of the whole chain
   const int g = blockIdx.y;
   const int M = it.n_cand * p.G;
-  const int count = it.tok_count;
+  int ntiles = 0;
+  for (int k = 0; k < nit; ++k) ntiles += tiles_of(p.items[i0 + k]);
 
   float m_run[RB], l_run[RB];
   f32x4_t acc[RB][8];
@@ -225,21 +265,11 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
     for (int db = 0; db < 8; ++db) acc[rb][db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  // Buffer resources over this item's rows of KV head g: loads of tokens past
-  // the item return zero (their scores are masked), so no clamping is needed.
-  // Offsets are 32-bit (the host keeps an item below 2^31 bytes).
   const uint32_t stride_b = p.tok_stride * 2;                      // bytes between tokens
-  const uint32_t nrec = (uint32_t)(count - 1) * stride_b + kRowBytes;
-  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride[it.chunk];
-  const __amdgpu_buffer_rsrc_t krs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k[it.chunk] + first), (short)0, (int)nrec, kBufferFlags);
-  const __amdgpu_buffer_rsrc_t vrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v[it.chunk] + first), (short)0, (int)nrec, kBufferFlags);
   const uint32_t voff = lq * stride_b + 16 * lr;                     // token lq, chunk lr
   unsigned char *qs = smem;
   unsigned char *ks = smem + MfmaLds<RB>::kQBytes + w * (2 * kTileBytes);
   unsigned char *vs = ks + kTileBytes;
-  const int ntiles = (count + kTile - 1) / kTile;
   const float sl2 = p.scale_log2;
 
   u32x4_t kr[8], vr[8];
@@ -247,13 +277,13 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   // whole offset goes in the VGPR operand: the buffer range check covers the
   // VGPR (and immediate) offset only, not the scalar one, and rows past the
   // item must come back as zeros rather than read beyond the buffer.
-  auto load_kv = [&](int tb) {
+  auto load_kv = [&](const NextTile &nx) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(krs, voff + (uint32_t)(tb + 4 * i) * stride_b, 0, 0);
+      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.krs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, 0);
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, voff + (uint32_t)(tb + 4 * i) * stride_b, 0, 0);
+      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.vrs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, 0);
   };
   // K operand read: row 16u + lr, chunk 4s + lq at position (4s + lq) ^ lr
   // V transpose read: row 4lq + lr/4 (+16), chunk 2db + (lr&3)/2, half lr&1
@@ -262,7 +292,9 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   const int vsw = 2 * (vrow & 7);
   const int vc0 = (lr & 3) >> 1;
 
-  auto tile = [&](int tb, auto prefetch) {
+  // one tile: tokens [tb, tb + 32) of an item with `count` tokens, already in
+  // kr / vr; `nx` is the tile to load next (unused for a wave's last tile)
+  auto tile = [&](int tb, int count, auto prefetch, const NextTile &nx) {
     constexpr bool kPrefetch = decltype(prefetch)::value;
     // stage K(i), V(i) in LDS, then issue the loads of the next tile
 #pragma unroll
@@ -271,7 +303,7 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
       *reinterpret_cast<u32x4_t *>(ks + t * kRowBytes + 16 * (lr ^ (t & 15))) = kr[i];
       *reinterpret_cast<u32x4_t *>(vs + t * kRowBytes + 16 * (lr ^ (2 * (t & 7)))) = vr[i];
     }
-    if constexpr (kPrefetch) load_kv(tb + kWaves * kTile);
+    if constexpr (kPrefetch) load_kv(nx);
     __builtin_amdgcn_sched_barrier(0);   // keep the prefetch here, ahead of the math
 
     // S^T = K Q^T
@@ -355,16 +387,37 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   // rows >= M are zero.  The Q^T operand (B[k = d][j = row]) of lane (lr, lq),
   // k-step s, is row lr's d-chunk 4s + lq.  The query loads are issued first,
   // then the first K/V tile, so staging Q waits only for the query rows.
+  // They are buffer loads over the whole Q tensor: a padding row (r >= M)
+  // gets an offset past the end and reads zero, so no load sits behind a
+  // branch (whose merge with the zero default would force an early wait).
   constexpr int kQPerThread = RB * 16 * 16 / 256;
+  const __amdgpu_buffer_rsrc_t qrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t *>(p.q), (short)0, (int)((uint32_t)p.st.R * kRowBytes), kBufferFlags);
   u32x4_t qv[kQPerThread];
 #pragma unroll
   for (int e = 0; e < kQPerThread; ++e) {
     const int c = threadIdx.x + 256 * e, r = c >> 4, ch = c & 15;
-    qv[e] = u32x4_t{0, 0, 0, 0};
-    if (r < M) qv[e] = reinterpret_cast<const u32x4_t *>(p.q + (size_t)global_row(p, it, g, r) * kHeadDim)[ch];
+    const uint32_t qoff = r < M ? (uint32_t)global_row(p, it, g, r) * kRowBytes + 16 * ch : 0x80000000u;
+    qv[e] = __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff, 0, 0);
   }
-  int t0 = w;
-  if (t0 < ntiles) load_kv(t0 * kTile);
+  // wave w takes the chain's tiles T = w, w + 4, ...  The first tile's loads
+  // are issued unconditionally (a wave without tiles loads through an empty
+  // resource, which reads nothing), so the wait for the query rows below
+  // does not have to include them.
+  int T = w;
+  TileCursor cur;
+  NextTile nx;
+  nx.krs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.q), (short)0, 0, kBufferFlags);
+  nx.vrs = nx.krs;
+  nx.tb = 0;
+  if (T < ntiles) {
+    seek(p, i0, nit, cur, T);
+    const Item ic = p.items[i0 + cur.k];
+    nx.krs = item_rsrc(p, ic, g, p.k);
+    nx.vrs = item_rsrc(p, ic, g, p.v);
+    nx.tb = (T - cur.base) * kTile;
+  }
+  load_kv(nx);
 #pragma unroll
   for (int e = 0; e < kQPerThread; ++e) {
     const int c = threadIdx.x + 256 * e, r = c >> 4, ch = c & 15;
@@ -372,9 +425,23 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
   }
   __syncthreads();
 
-  if (t0 < ntiles) {
-    for (; t0 + kWaves < ntiles; t0 += kWaves) tile(t0 * kTile, std::integral_constant<bool, true>{});
-    tile(t0 * kTile, std::integral_constant<bool, false>{});
+  if (T < ntiles) {
+    int tb = nx.tb;
+    int count = p.items[i0 + cur.k].tok_count;
+    for (; T + kWaves < ntiles; T += kWaves) {
+      const int kprev = cur.k;
+      seek(p, i0, nit, cur, T + kWaves);
+      if (cur.k != kprev) {
+        const Item in = p.items[i0 + cur.k];
+        nx.krs = item_rsrc(p, in, g, p.k);
+        nx.vrs = item_rsrc(p, in, g, p.v);
+      }
+      nx.tb = (T + kWaves - cur.base) * kTile;
+      tile(tb, count, std::integral_constant<bool, true>{}, nx);
+      tb = nx.tb;
+      count = p.items[i0 + cur.k].tok_count;
+    }
+    tile(tb, count, std::integral_constant<bool, false>{}, nx);
   }
 
   // wave partials -> LDS
@@ -412,10 +479,14 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
   const int lane = threadIdx.x & 63;
   const int c = lane & 15;
   const int tg = lane >> 4;
-  const Item it = p.items[blockIdx.x];
+  const uint32_t unit = p.units[blockIdx.x];
+  const int i0 = unit & 0xffff;
+  const int nit = unit >> 16;
+  const Item it = p.items[i0];          // request, slot and flags of the whole chain
   const int g = blockIdx.y;
   const int M = it.n_cand * p.G;
-  const int count = it.tok_count;
+  int ntiles = 0;
+  for (int k = 0; k < nit; ++k) ntiles += tiles_of(p.items[i0 + k]);
 
   float qf[MAXR][8];
 #pragma unroll
@@ -441,32 +512,26 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
     for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
   }
   const uint32_t stride_b = p.tok_stride * 2;
-  const uint32_t nrec = (uint32_t)(count - 1) * stride_b + 2 * kHeadDim;
-  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride[it.chunk];
-  const __amdgpu_buffer_rsrc_t krs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k[it.chunk] + first), (short)0, (int)nrec, kBufferFlags);
-  const __amdgpu_buffer_rsrc_t vrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v[it.chunk] + first), (short)0, (int)nrec, kBufferFlags);
   const uint32_t voff = tg * stride_b + 16 * c;
-  const int ntiles = (count + kTile - 1) / kTile;
   const float sl2 = p.scale_log2;
 
   // coalesced loads (4 token rows per instruction); tokens past the item read 0
   u32x4_t kr[8], vr[8];
   // the whole offset goes in the range-checked VGPR operand (see the MFMA kernel)
-  auto load_k = [&](int tb) {
+  auto load_k = [&](const NextTile &nx) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(krs, voff + (uint32_t)(tb + 4 * i) * stride_b, 0, 0);
+      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.krs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, 0);
   };
-  auto load_v = [&](int tb) {
+  auto load_v = [&](const NextTile &nx) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, voff + (uint32_t)(tb + 4 * i) * stride_b, 0, 0);
+      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.vrs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, 0);
   };
-  // one tile per iteration; the next tile's K is issued after the scores, its
-  // V after the PV update; the last tile is peeled (unconditional prefetch)
-  auto tile = [&](int tb, auto prefetch) {
+  // one tile per iteration (tokens [tb, tb + 32) of an item with `count`
+  // tokens); the next tile's K is issued after the scores, its V after the
+  // PV update; the last tile is peeled (unconditional prefetch)
+  auto tile = [&](int tb, int count, auto prefetch, const NextTile &nx) {
     constexpr bool more = decltype(prefetch)::value;
     float x[8][MAXR];
 #pragma unroll
@@ -487,7 +552,7 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
         x[i][r] = valid ? d * sl2 : kNegInf;
       }
     }
-    if constexpr (more) load_k(tb + kWaves * kTile);
+    if constexpr (more) load_k(nx);
 #pragma unroll
     for (int r = 0; r < MAXR; ++r) {
       float mx = kNegInf;
@@ -520,14 +585,38 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(x[i][r], vf[e], acc[r][e]);
     }
-    if constexpr (more) load_v(tb + kWaves * kTile);
+    if constexpr (more) load_v(nx);
   };
-  int t0 = w;
-  if (t0 < ntiles) {
-    load_k(t0 * kTile);
-    load_v(t0 * kTile);
-    for (; t0 + kWaves < ntiles; t0 += kWaves) tile(t0 * kTile, std::integral_constant<bool, true>{});
-    tile(t0 * kTile, std::integral_constant<bool, false>{});
+  // wave w takes the chain's tiles T = w, w + 4, ...
+  int T = w;
+  if (T < ntiles) {
+    TileCursor cur;
+    NextTile nx;
+    seek(p, i0, nit, cur, T);
+    {
+      const Item ic = p.items[i0 + cur.k];
+      nx.krs = item_rsrc(p, ic, g, p.k);
+      nx.vrs = item_rsrc(p, ic, g, p.v);
+      nx.tb = (T - cur.base) * kTile;
+    }
+    load_k(nx);
+    load_v(nx);
+    int tb = nx.tb;
+    int count = p.items[i0 + cur.k].tok_count;
+    for (; T + kWaves < ntiles; T += kWaves) {
+      const int kprev = cur.k;
+      seek(p, i0, nit, cur, T + kWaves);
+      if (cur.k != kprev) {
+        const Item in = p.items[i0 + cur.k];
+        nx.krs = item_rsrc(p, in, g, p.k);
+        nx.vrs = item_rsrc(p, in, g, p.v);
+      }
+      nx.tb = (T + kWaves - cur.base) * kTile;
+      tile(tb, count, std::integral_constant<bool, true>{}, nx);
+      tb = nx.tb;
+      count = p.items[i0 + cur.k].tok_count;
+    }
+    tile(tb, count, std::integral_constant<bool, false>{}, nx);
   }
 
   // reduce over the token groups, partials -> LDS
@@ -667,7 +756,7 @@ __global__ void __launch_bounds__(256) finalize_kernel(const FinalParams p) {
 }  // namespace
 
 hipError_t launch_chunk_mfma(const ChunkParams &p, int row_blocks, hipStream_t s) {
-  const dim3 grid(p.num_items, p.Hkv);
+  const dim3 grid(p.num_units, p.Hkv);
   if (row_blocks == 1)
     hipLaunchKernelGGL(chunk_attn_mfma<1>, grid, dim3(256), 0, s, p);
   else
@@ -676,7 +765,7 @@ hipError_t launch_chunk_mfma(const ChunkParams &p, int row_blocks, hipStream_t s
 }
 
 hipError_t launch_chunk_valu(const ChunkParams &p, hipStream_t s) {
-  hipLaunchKernelGGL(chunk_attn_valu<kMaxValuRows>, dim3(p.num_items, p.Hkv), dim3(256), 0, s, p);
+  hipLaunchKernelGGL(chunk_attn_valu<kMaxValuRows>, dim3(p.num_units, p.Hkv), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

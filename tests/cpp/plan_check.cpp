@@ -1,0 +1,191 @@
+// CPU check of the history-call planner together with the chunk kernels' tile
+// traversal: every token of every request is visited exactly once per KV
+// head, every buffer resource stays inside its chunk, chains are
+// single-request and single-slot, slots and fresh flags are consistent.
+// The kernel launchers are stubs that record the launch tables.
+#include "ss_kernels.h"
+#include "specstream.h"
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <random>
+#include <vector>
+#include <set>
+
+namespace {
+struct Rec { std::vector<ss::Item> items; std::vector<uint32_t> units; int kind; };
+std::vector<Rec> g_recs;
+const ss::ChunkParams *g_last = nullptr;
+}
+
+namespace ss {
+static void rec(const ChunkParams &p, int kind) {
+  Rec r;
+  r.items.assign(p.items, p.items + p.num_items);
+  r.units.assign(p.units, p.units + p.num_units);
+  r.kind = kind;
+  if (p.num_units < 1 || p.num_units > kMaxUnits || p.num_items < 1 || p.num_items > kMaxItems) { printf("bad counts\n"); exit(1); }
+  g_recs.push_back(r);
+  g_last = &p;
+}
+hipError_t launch_chunk_mfma(const ChunkParams &p, int rb, hipStream_t) { rec(p, rb); return hipSuccess; }
+hipError_t launch_chunk_valu(const ChunkParams &p, hipStream_t) { rec(p, 0); return hipSuccess; }
+hipError_t launch_finalize(const FinalParams &, hipStream_t) { return hipSuccess; }
+}
+
+static int tiles_of(const ss::Item &it) { return (it.tok_count + ss::kTile - 1) / ss::kTile; }
+
+static int fails = 0;
+#define CHECK(c, ...) do { if (!(c)) { printf("FAIL %s:%d: ", __FILE__, __LINE__); printf(__VA_ARGS__); printf("\n"); if (++fails > 20) exit(1); } } while (0)
+
+// emulate one history call: returns per-request slot set written
+static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, const std::vector<std::vector<int>> &lens,
+                       int split, int layout, int mfma_min_rows, std::vector<int> &slots_used, ss_round *r) {
+  const int nch = (int)lens.size();
+  std::vector<int32_t> flat;
+  std::vector<long> tot(nch, 0);
+  for (int c = 0; c < nch; ++c) for (int b = 0; b < B; ++b) { flat.push_back(lens[c][b]); tot[c] += lens[c][b]; }
+  std::vector<const void *> kp(nch), vp(nch);
+  // fake aligned chunk pointers; never dereferenced
+  for (int c = 0; c < nch; ++c) { kp[c] = (const void *)(uintptr_t)(0x100000000ull * (c + 1)); vp[c] = (const void *)(uintptr_t)(0x100000000ull * (c + 1) + 0x80000000ull); }
+  g_recs.clear();
+  ss_status s = ss_attend_history_chunks(r, nch, kp.data(), vp.data(), flat.data(), nullptr, nullptr, nullptr);
+  CHECK(s == SS_OK, "status %d: %s", s, ss_last_error());
+  if (s != SS_OK) return;
+  // coverage[b][c] token counts
+  std::vector<std::vector<std::vector<int>>> cov(B, std::vector<std::vector<int>>(nch));
+  for (int b = 0; b < B; ++b) for (int c = 0; c < nch; ++c) cov[b][c].assign(lens[c][b], 0);
+  std::map<std::pair<int,int>, int> slot_writes;   // (request, slot) -> units
+  const int G = Hq / Hkv;
+  std::vector<int> off_rows(B, 0);
+  for (int b = 1; b < B; ++b) off_rows[b] = off_rows[b - 1] + ncand[b - 1];
+  for (auto &rc : g_recs) {
+    for (size_t u = 0; u < rc.units.size(); ++u) {
+      const int i0 = rc.units[u] & 0xffff, nit = rc.units[u] >> 16;
+      CHECK(nit >= 1 && nit <= ss::kMaxChain && i0 + nit <= (int)rc.items.size(), "unit table");
+      const ss::Item &it = rc.items[i0];
+      int b = -1;
+      for (int bb = 0; bb < B; ++bb) if (off_rows[bb] == it.q_row0) b = bb;
+      CHECK(b >= 0, "q_row0");
+      const int M = it.n_cand * G;
+      const int want_kind = (M < (mfma_min_rows ? mfma_min_rows : 5) && M <= 4) ? 0 : (M <= 16 ? 1 : 2);
+      CHECK(rc.kind == want_kind, "kernel kind %d want %d (M=%d)", rc.kind, want_kind, M);
+      int ntiles = 0;
+      long toks = 0;
+      for (int k = 0; k < nit; ++k) {
+        const ss::Item &ik = rc.items[i0 + k];
+        CHECK(ik.q_row0 == it.q_row0 && ik.slot == it.slot && ik.flags == it.flags && ik.n_cand == it.n_cand, "chain mixes");
+        CHECK(ik.tok_count >= 1, "empty item");
+        CHECK(ik.chunk < nch, "chunk index");
+        ntiles += tiles_of(ik);
+        toks += ik.tok_count;
+        // the item is request b's tokens of chunk ik.chunk
+        long ofs = 0;
+        for (int bb = 0; bb < b; ++bb) ofs += lens[ik.chunk][bb];
+        CHECK(ik.tok_begin >= ofs && ik.tok_begin + ik.tok_count <= ofs + lens[ik.chunk][b], "item outside request range");
+        // buffer resource bounds for every head: [first, first + nrec) inside the chunk
+        const long stride = layout == SS_KV_TOKEN_MAJOR ? (long)Hkv * 128 : 128;
+        const long hstride = layout == SS_KV_TOKEN_MAJOR ? 128 : tot[ik.chunk] * 128;
+        for (int g = 0; g < Hkv; ++g) {
+          const long first = (long)ik.tok_begin * stride + (long)g * hstride;
+          const long nrec = (long)(ik.tok_count - 1) * stride * 2 + 256;
+          CHECK(first * 2 + nrec <= tot[ik.chunk] * Hkv * 256, "rsrc past chunk");
+          CHECK(nrec < (1L << 31), "nrec 32-bit");
+        }
+      }
+      CHECK(toks >= 1, "empty unit");
+      slot_writes[{b, it.slot}]++;
+      CHECK(((it.flags & ss::kSlotFresh) != 0) == (it.slot >= slots_used[b]), "fresh flag");
+      // emulate the 4 waves' traversal (same as the kernels)
+      for (int w = 0; w < ss::kWaves; ++w) {
+        int T = w;
+        int ck = 0, cbase = 0;
+        auto seek = [&](int TT) {
+          while (ck + 1 < nit && TT - cbase >= tiles_of(rc.items[i0 + ck])) { cbase += tiles_of(rc.items[i0 + ck]); ++ck; }
+        };
+        for (; T < ntiles; T += ss::kWaves) {
+          seek(T);
+          const ss::Item &ic = rc.items[i0 + ck];
+          const int tb = (T - cbase) * ss::kTile;
+          CHECK(tb >= 0 && tb < ic.tok_count, "tile outside item (tb %d count %d)", tb, ic.tok_count);
+          long ofs = 0;
+          for (int bb = 0; bb < b; ++bb) ofs += lens[ic.chunk][bb];
+          for (int t = tb; t < tb + ss::kTile && t < ic.tok_count; ++t) cov[b][ic.chunk][ic.tok_begin - ofs + t]++;
+        }
+      }
+    }
+  }
+  for (int b = 0; b < B; ++b)
+    for (int c = 0; c < nch; ++c)
+      for (int t = 0; t < lens[c][b]; ++t) CHECK(cov[b][c][t] == 1, "token b=%d c=%d t=%d visited %d times", b, c, t, cov[b][c][t]);
+  for (auto &kv : slot_writes) CHECK(kv.second == 1, "slot (%d,%d) written by %d units", kv.first.first, kv.first.second, kv.second);
+  for (auto &kv : slot_writes) CHECK(kv.first.second < ss::kNumSlots, "slot index");
+  for (int b = 0; b < B; ++b) {
+    int mx = -1;
+    for (auto &kv : slot_writes) if (kv.first.first == b) mx = std::max(mx, kv.first.second);
+    for (int s2 = 0; s2 <= mx; ++s2) CHECK(slot_writes.count({b, s2}), "slot gap b=%d s=%d", b, s2);
+    slots_used[b] = std::max(slots_used[b], mx + 1);
+  }
+}
+
+static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> ncand, std::vector<int> hist, int S,
+                     int split, int layout, int batch, int mfma_min_rows = 0) {
+  const int nch = [&] { int m = 0; for (int h : hist) m = std::max(m, (h + S - 1) / S); return m; }();
+  std::vector<std::vector<int>> lens(nch, std::vector<int>(B));
+  long maxc = 1;
+  for (int c = 0; c < nch; ++c) { long t = 0; for (int b = 0; b < B; ++b) { lens[c][b] = std::max(0, std::min(S, hist[b] - c * S)); t += lens[c][b]; } maxc = std::max(maxc, t); }
+  ss_round_desc d{};
+  d.num_requests = B; d.num_q_heads = Hq; d.num_kv_heads = Hkv; d.head_dim = 128; d.softmax_scale = 0.088f;
+  d.num_cand = ncand.data(); d.max_chunk_tokens = (int)maxc; d.split_tokens = split; d.mfma_min_rows = mfma_min_rows; d.kv_layout = layout;
+  ss_round *r = nullptr;
+  size_t ws = ss_round_workspace_bytes(&d);
+  ss_status s = ss_round_init(&r, &d, (const void *)0x7f0000000000ull, (void *)0x7f1000000000ull, ws, nullptr);
+  if (s != SS_OK) { printf("%s: init failed %s\n", name, ss_last_error()); fails++; return; }
+  std::vector<int> used(B, 0);
+  const int before = fails;
+  // chunk batches
+  for (int c0 = 0; c0 < nch; c0 += batch) {
+    std::vector<std::vector<int>> part(lens.begin() + c0, lens.begin() + std::min(nch, c0 + batch));
+    long t = 0;
+    for (auto &row : part) for (int x : row) t += x;
+    // the library sizes max_chunk_tokens per chunk; a batched call checks each chunk
+    check_call(B, Hq, Hkv, ncand, part, split, layout, mfma_min_rows, used, r);
+  }
+  ss_round_destroy(r);
+  printf("%-44s %s (launches in last call: %zu)\n", name, fails == before ? "ok" : "FAILED", g_recs.size());
+}
+
+int main() {
+  std::mt19937 rng(7);
+  for (int layout : {SS_KV_TOKEN_MAJOR, SS_KV_HEAD_MAJOR}) {
+    scenario("config1 per-chunk", 1, 8, 2, {5}, {4096}, 1024, 0, layout, 1);
+    scenario("config1 split 32", 1, 8, 2, {5}, {4096}, 1024, 32, layout, 1);
+    scenario("config1 split 96", 1, 8, 2, {5}, {4096}, 1024, 96, layout, 1);
+    scenario("config1 batched", 1, 8, 2, {5}, {4096}, 1024, 0, layout, 4);
+    scenario("config2 per-chunk", 1, 32, 8, {5}, {16384}, 2048, 0, layout, 1);
+    scenario("config3 batched 8", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8);
+    scenario("config3 per-chunk", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 1);
+    scenario("config3 batched 3", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 3);
+    scenario("config3 split 2048 batched", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 2048, layout, 8);
+    scenario("config5 per-chunk", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 1);
+    scenario("config5 batched 16", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 16);
+    scenario("many units (8192 chains)", 256, 8, 2, std::vector<int>(256, 3), std::vector<int>(256, 4096), 512, 128, layout, 8);
+    scenario("many items (chains of 16)", 128, 8, 2, std::vector<int>(128, 2), std::vector<int>(128, 8192), 32, 512, layout, 32);
+    for (int rep = 0; rep < 40; ++rep) {
+      const int B = 1 + rng() % 64;
+      std::vector<int> nc(B), h(B);
+      for (int b = 0; b < B; ++b) { nc[b] = 1 + rng() % 8; h[b] = (rng() % 4 == 0) ? (int)(rng() % 70) : (int)(rng() % 66000); }
+      const int S = 32 * (1 + rng() % 256);
+      const int split = (rng() % 3 == 0) ? 32 * (1 + rng() % 64) : 0;
+      int nch = 0; for (int x : h) nch = std::max(nch, (x + S - 1) / S);
+      if (nch == 0) continue;
+      const int batch = 1 + rng() % 32;
+      const int hq = (rng() % 2) ? 32 : 8, hkv = hq == 32 ? 8 : 2;
+      char nm[64]; snprintf(nm, sizeof nm, "random %d B=%d S=%d split=%d batch=%d", rep, B, S, split, batch);
+      scenario(nm, B, hq, hkv, nc, h, S, split, layout, batch, (int)(rng() % 6));
+    }
+  }
+  printf("%s\n", fails ? "FAILURES" : "all ok");
+  return fails ? 1 : 0;
+}
