@@ -185,6 +185,170 @@ def streamed_round(torch, H, w, b, chunks, stream, rounds: int):
     return t_stream, t_h2d, host.total_bytes, same
 
 
+def round_times(torch, H, b, chunks, stream, rounds: int, batch: int, flush=None):
+    """Device time of each of `rounds` rounds (events around every round; with
+    `flush`, a cache-evicting fill runs between rounds, outside the events)."""
+    evs = []
+    for _ in range(rounds):
+        if flush is not None:
+            with torch.cuda.stream(stream):
+                flush.add_(1)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        H.run_round(b, chunks, stream.cuda_stream, batch=batch)
+        e1.record(stream)
+        evs.append((e0, e1))
+    torch.cuda.synchronize()
+    return sorted(e0.elapsed_time(e1) / 1e3 for e0, e1 in evs)
+
+
+def pct(xs, q):
+    i = min(len(xs) - 1, max(0, int(round(q * (len(xs) - 1)))))
+    return xs[i]
+
+
+def config_table(torch, H, ss, W, stream, layout: int, rounds: int):
+    """In-HBM round of every other configuration (one batched history call;
+    configurations whose history fits the 256 MB last-level cache get a
+    512 MiB cache-evicting fill between rounds, outside the timed events)."""
+    table = {}
+    for cfg in (1, 2, 4, 5):
+        w = W.workload(cfg)
+        log(f"bench: config {cfg} ({w.name}) in HBM")
+        b = H.RoundBuffers(w, kv_layout=layout)
+        chunks = H.hbm_history(w, kv_layout=layout)
+        flush = torch.zeros(1 << 27, dtype=torch.int32, device="cuda") if w.history_kv_bytes() < (1 << 28) else None
+        torch.cuda.synchronize()
+        batch = w.num_chunks
+        round_times(torch, H, b, chunks, stream, 2, batch, flush)
+        t = round_times(torch, H, b, chunks, stream, rounds, batch, flush)
+        kv = w.algorithmic_kv_bytes()
+        p50 = pct(t, 0.5)
+        table[str(cfg)] = {"workload": w.name, "kv_bytes_per_round": kv, "rounds": rounds,
+                           "round_us_p10": round(pct(t, 0.1) * 1e6, 2), "round_us_p50": round(p50 * 1e6, 2),
+                           "round_us_p90": round(pct(t, 0.9) * 1e6, 2),
+                           "effective_KV_GBs_p50": round(kv / p50 / 1e9, 2),
+                           "pct_of_hbm_peak_p50": round(100.0 * kv / p50 / 1e9 / HBM_PEAK_GBS, 2),
+                           "cache_flushed_between_rounds": flush is not None}
+        del b, chunks, flush
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    return table
+
+
+def full_depth_streamed(torch, H, ss, W, stream, layout: int, layers: int):
+    """Config 5 end to end: `layers` layers (each its own queries) whose
+    shared 16 GiB history streams from pinned host memory through one
+    continuous two-slot pipeline."""
+    w = W.workload(5)
+    log(f"bench: full-depth streamed round, {layers} layers: filling pinned host history")
+    host = H.HostHistory(w, kv_layout=layout)
+    pipe = H.Pipeline(host.max_chunk_bytes())
+    try:
+        bufs = [H.RoundBuffers(w, layer=l, kv_layout=layout) for l in range(layers)]
+        torch.cuda.synchronize()
+        H.run_round_streamed(bufs[0], host, pipe, stream.cuda_stream)     # warm-up layer
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for b in bufs:
+            H.run_round_streamed(b, host, pipe, stream.cuda_stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / 1e3
+    finally:
+        pipe.close()
+    h2d = host.total_bytes * layers
+    return {"workload": w.name, "layers": layers, "round_s": round(t, 4), "per_layer_ms": round(t / layers * 1e3, 3),
+            "h2d_bytes": h2d, "host_link_GBs": round(h2d / t / 1e9, 2),
+            "in_hbm_equivalent_KV_GBs": round(w.algorithmic_kv_bytes() * layers / t / 1e9, 2)}
+
+
+def ablation(torch, H, ss, W, stream, layout: int):
+    """Kernel-level analogue of the paper's K1 -> K2 -> K3 ablation (Sec. 5.3.1):
+    K1 restore the whole history to HBM, then attend; K2 stream chunk by chunk
+    through one staging slot (upload and attention alternate); K3 the
+    two-slot pipeline (upload of chunk j+1 overlaps attention on chunk j)."""
+    rows = []
+    for ctx in (16384, 32768):
+        for nreq in (1, 4, 8, 16):
+            w = W.custom([ctx] * nreq, [6] * nreq, num_q_heads=32, num_kv_heads=8, chunk_tokens=4096, seed_base=5)
+            log(f"bench: ablation ctx {ctx} requests {nreq}")
+            host = H.HostHistory(w, kv_layout=layout)
+            b = H.RoundBuffers(w, kv_layout=layout)
+            res = {}
+            # K1: restore everything, then one batched attention call
+            dev = [torch.empty(host.sizes[j], dtype=torch.uint8, device="cuda") for j in range(w.num_chunks)]
+            copy = torch.cuda.Stream()
+            done = ss.ss_event_create()
+            try:
+                def k1():
+                    for j in range(w.num_chunks):
+                        ss.ss_upload_chunk(dev[j].data_ptr(), host.chunk_ptr(j), host.sizes[j], copy.cuda_stream,
+                                           None, done if j == w.num_chunks - 1 else None)
+                    r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream.cuda_stream)
+                    try:
+                        half = [host.sizes[j] // 2 for j in range(w.num_chunks)]
+                        ss.ss_attend_history_chunks(r, [dev[j].data_ptr() for j in range(w.num_chunks)],
+                                                    [dev[j].data_ptr() + half[j] for j in range(w.num_chunks)],
+                                                    [w.chunk_lens(j) for j in range(w.num_chunks)], done, None,
+                                                    stream.cuda_stream)
+                        ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream.cuda_stream)
+                        ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream.cuda_stream)
+                    finally:
+                        ss.ss_round_destroy(r)
+
+                def k2():
+                    slot = dev[0]
+                    ready, free = ss.ss_event_create(), ss.ss_event_create()
+                    try:
+                        r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream.cuda_stream)
+                        try:
+                            for j in range(w.num_chunks):
+                                half = host.sizes[j] // 2
+                                ss.ss_upload_chunk(slot.data_ptr(), host.chunk_ptr(j), host.sizes[j], copy.cuda_stream,
+                                                   free if j else None, ready)
+                                ss.ss_attend_history_chunk(r, slot.data_ptr(), slot.data_ptr() + half, w.chunk_lens(j),
+                                                           ready, free, stream.cuda_stream)
+                            ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream.cuda_stream)
+                            ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream.cuda_stream)
+                        finally:
+                            ss.ss_round_destroy(r)
+                        torch.cuda.synchronize()
+                    finally:
+                        ss.ss_event_destroy(ready)
+                        ss.ss_event_destroy(free)
+
+                pipe = H.Pipeline(host.max_chunk_bytes())
+                try:
+                    def k3():
+                        H.run_round_streamed(b, host, pipe, stream.cuda_stream)
+
+                    for name, fn in (("K1_restore_then_attend", k1), ("K2_stream_no_overlap", k2),
+                                     ("K3_two_slot_pipeline", k3)):
+                        fn()
+                        torch.cuda.synchronize()
+                        ts = []
+                        for _ in range(3):
+                            t0 = time.perf_counter()
+                            fn()
+                            torch.cuda.synchronize()
+                            ts.append(time.perf_counter() - t0)
+                        res[name + "_ms"] = round(min(ts) * 1e3, 3)
+                finally:
+                    pipe.close()
+            finally:
+                ss.ss_event_destroy(done)
+            res.update({"context": ctx, "requests": nreq, "h2d_bytes": host.total_bytes})
+            res["K3_over_K1"] = round(res["K1_restore_then_attend_ms"] / res["K3_two_slot_pipeline_ms"], 3)
+            rows.append(res)
+            del host, b, dev
+            torch.cuda.empty_cache()
+    return rows
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -204,6 +368,12 @@ def main() -> int:
                     help="only time the history-chunk launches (for profiler runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 1 GiB device-to-device copy (counter calibration)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the in-HBM rounds of the other configurations")
+    ap.add_argument("--full-depth", type=int, default=0, metavar="LAYERS",
+                    help="also time config 5 end to end: LAYERS layers streamed through one pipeline")
+    ap.add_argument("--ablation", action="store_true",
+                    help="also run the K1/K2/K3 (restore / stream / stream+prefetch) comparison")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); "
@@ -248,6 +418,7 @@ def main() -> int:
     step_s = dt / args.steps
     kv_bytes = w.algorithmic_kv_bytes()
     value = kv_bytes * args.steps / dt / 1e9
+    per_round = round_times(torch, H, b, chunks, stream, args.steps, batch)
 
     log("bench: per-launch timing of the history kernel")
     times = per_launch_times(torch, ss, b, chunks, stream, 5, batch)
@@ -298,6 +469,7 @@ def main() -> int:
                         f"{w.num_chunks} chunks of {w.chunk_tokens}, {w.num_cand[0] if len(set(w.num_cand)) == 1 else 'ragged'} "
                         f"candidate queries, history resident in HBM ({args.kv_layout}-major chunks)",
             "round_latency_ms": round(step_s * 1e3, 4),
+            "round_latency_us_p10_p50_p90": [round(pct(per_round, q) * 1e6, 2) for q in (0.1, 0.5, 0.9)],
             "chunks_per_history_call": batch,
             "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
             "kv_bytes_per_round": kv_bytes,
@@ -333,6 +505,14 @@ def main() -> int:
             "attention_hidden_frac": round(max(0.0, min(1.0, (t_h2d + step_s - t_stream) / step_s)), 4),
             "bitwise_equal_to_in_hbm": same,
         }
+    if not args.no_configs and args.config == 3:
+        del chunks
+        torch.cuda.empty_cache()
+        out["other_configs_in_hbm"] = config_table(torch, H, ss, W, stream, layout, max(5, args.steps // 2))
+    if args.full_depth > 0:
+        out["full_depth_streamed"] = full_depth_streamed(torch, H, ss, W, stream, layout, args.full_depth)
+    if args.ablation:
+        out["ablation_k1_k2_k3"] = ablation(torch, H, ss, W, stream, layout)
     print(json.dumps(out), flush=True)
     return 0
 

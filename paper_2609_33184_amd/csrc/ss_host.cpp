@@ -179,14 +179,22 @@ struct Plan {
 // sequence) into pieces of `piece` tokens; a piece is a chain of at most
 // kMaxChain ranges (a chunk boundary starts a new range) and gets its own
 // state slot.  Returns false if a request would need more than kNumSlots.
-bool build_plan(const ss_round *r, int nchunks, const int32_t *len, long piece, Plan *plan) {
+// Kernel variant of request b: 0 = VALU (few rows per KV head), 1 = MFMA with
+// one 16-row block, 2 = MFMA with two.
+int variant_of(const ss_round *r, int b) {
   const int min_rows = r->mfma_min_rows > 0 ? r->mfma_min_rows : kDefaultMfmaMinRows;
+  const int M = r->n_cand[b] * r->G;
+  return (M < min_rows && M <= ss::kMaxValuRows) ? 0 : (M <= 16) ? 1 : 2;
+}
+
+bool build_plan(const ss_round *r, int nchunks, const int32_t *len, const long piece_of[3], Plan *plan) {
   *plan = Plan();
   plan->slots_after = r->slots_used;
   std::vector<long> off(nchunks, 0);   // first token of request b in chunk c
   for (int b = 0; b < r->B; ++b) {
-    const int M = r->n_cand[b] * r->G;
-    Chains *dst = (M < min_rows && M <= ss::kMaxValuRows) ? &plan->valu : (M <= 16) ? &plan->rb1 : &plan->rb2;
+    const int var = variant_of(r, b);
+    Chains *dst = var == 0 ? &plan->valu : var == 1 ? &plan->rb1 : &plan->rb2;
+    const long piece = piece_of[var];
     int slot = 0;
     long filled = 0;      // tokens in the open chain
     int ranges = 0;       // items in the open chain
@@ -243,22 +251,28 @@ void sort_chains(Chains *ch) {
 
 ss_status plan_chunks(const ss_round *r, int nchunks, const int32_t *len, const std::vector<long> &tot,
                       Plan *plan) {
-  long total = 0;
-  for (long t : tot) total += t;
-  long piece;
-  if (r->split_tokens > 0) {
-    piece = r->split_tokens;
-  } else {
-    const long work = total * r->Hkv;
-    piece = (work + kTargetWorkgroups - 1) / kTargetWorkgroups;
-    piece = std::min<long>(kMaxAutoPiece, std::max<long>(kMinPiece, align_up(piece, ss::kTile)));
-  }
+  (void)tot;
+  // each kernel variant is its own launch: size its pieces from its own tokens
+  long total[3] = {0, 0, 0};
+  for (int b = 0; b < r->B; ++b)
+    for (int c = 0; c < nchunks; ++c) total[variant_of(r, b)] += len[(size_t)c * r->B + b];
   const long pmax = max_piece_tokens(r);
-  piece = std::min(piece, pmax);
+  long piece[3];
+  for (int v = 0; v < 3; ++v) {
+    if (r->split_tokens > 0) {
+      piece[v] = r->split_tokens;
+    } else {
+      const long work = total[v] * r->Hkv;
+      piece[v] = (work + kTargetWorkgroups - 1) / kTargetWorkgroups;
+      piece[v] = std::min<long>(kMaxAutoPiece, std::max<long>(kMinPiece, align_up(piece[v], ss::kTile)));
+    }
+    piece[v] = std::min(piece[v], pmax);
+  }
   // every request must fit its pieces into the slots
   while (!build_plan(r, nchunks, len, piece, plan)) {
-    if (piece >= pmax) return fail(SS_ERR_INVALID_ARGUMENT, "too many tokens per request for one history call");
-    piece = std::min(pmax, piece * 2);
+    if (piece[0] >= pmax && piece[1] >= pmax && piece[2] >= pmax)
+      return fail(SS_ERR_INVALID_ARGUMENT, "too many tokens per request for one history call");
+    for (int v = 0; v < 3; ++v) piece[v] = std::min(pmax, piece[v] * 2);
   }
   sort_chains(&plan->valu);
   sort_chains(&plan->rb1);

@@ -660,7 +660,7 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
 // independent chains; the frontier terms are summed first, then each group
 // of slots is folded in with the rescaled update of Eq. 14.
 // ---------------------------------------------------------------------------
-constexpr int kFinGroup = 8;
+constexpr int kFinGroup = 16;
 
 __global__ void __launch_bounds__(256) finalize_kernel(const FinalParams p) {
   const int w = threadIdx.x >> 6;
