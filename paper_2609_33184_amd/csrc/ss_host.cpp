@@ -40,8 +40,11 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // has no hand-over between them; aim for one workgroup per CU (256 on
 // MI355X) per launch.  A piece may span chunks of a batched call.  Measured
 // on 16 x 32768 tokens, 8 KV heads: 1024 workgroups of 4096 tokens 394 us,
-// 512 of 8192 384 us, 256 of 16384 381 us per round.
+// 512 of 8192 384 us, 256 of 16384 381 us per round.  On 64 requests of
+// 2048..65536 tokens, pieces of about an eighth of the per-CU share balance
+// best (4096 tokens: 801 us, 8192: 826 us, 16384: 864 us, 36864: 915 us).
 constexpr long kTargetWorkgroups = 256;
+constexpr long kRaggedSplit = 8;   // units per CU when request lengths differ
 constexpr int kMinPiece = 256;
 constexpr int kMaxAutoPiece = 32768;
 constexpr int kDefaultMfmaMinRows = ss::kMaxValuRows + 1;
@@ -157,11 +160,12 @@ ss_status check_history_args(const ss_round *r, int nchunks, const void *const *
   return SS_OK;
 }
 
-// Work of one history call for one kernel variant: chains of items, chain c
-// = items[start[c] .. start[c + 1]) (one request, one state slot).
+// Work of one history call: chains of items, chain c = items[start[c] ..
+// start[c + 1]) (one request, one state slot), attended by kernel body kind[c].
 struct Chains {
   std::vector<ss::Item> items;
   std::vector<uint32_t> start{0};
+  std::vector<uint8_t> kind;
   size_t size() const { return start.size() - 1; }
   long tokens(size_t c) const {
     long n = 0;
@@ -171,47 +175,52 @@ struct Chains {
 };
 
 struct Plan {
-  Chains valu, rb1, rb2;
+  Chains chains;
   std::vector<int32_t> slots_after;   // per request: slots in use after this call
 };
 
-// Cut every request's tokens of this call (its ranges in chunk order, as one
-// sequence) into pieces of `piece` tokens; a piece is a chain of at most
-// kMaxChain ranges (a chunk boundary starts a new range) and gets its own
-// state slot.  Returns false if a request would need more than kNumSlots.
-// Kernel variant of request b: 0 = VALU (few rows per KV head), 1 = MFMA with
-// one 16-row block, 2 = MFMA with two.
-int variant_of(const ss_round *r, int b) {
+// Kernel body of request b's units: VALU for few rows per KV head, else MFMA
+// with one or two 16-row blocks.
+int kind_of(const ss_round *r, int b) {
   const int min_rows = r->mfma_min_rows > 0 ? r->mfma_min_rows : kDefaultMfmaMinRows;
   const int M = r->n_cand[b] * r->G;
-  return (M < min_rows && M <= ss::kMaxValuRows) ? 0 : (M <= 16) ? 1 : 2;
+  return (M < min_rows && M <= ss::kMaxValuRows) ? ss::kUnitValu : (M <= 16) ? ss::kUnitMfma1 : ss::kUnitMfma2;
 }
 
-bool build_plan(const ss_round *r, int nchunks, const int32_t *len, const long piece_of[3], Plan *plan) {
+// Cut every request's tokens of this call (its ranges in chunk order, as one
+// sequence) into n_b = ceil(L_b / piece) pieces of equal size (a multiple of
+// the tile, the last one shorter); a piece is a chain of at most kMaxChain
+// ranges (a chunk boundary starts a new range) and gets its own state slot.
+// Returns false if a request would need more than kNumSlots slots.
+bool build_plan(const ss_round *r, int nchunks, const int32_t *len, long piece, Plan *plan) {
   *plan = Plan();
   plan->slots_after = r->slots_used;
+  Chains *dst = &plan->chains;
   std::vector<long> off(nchunks, 0);   // first token of request b in chunk c
   for (int b = 0; b < r->B; ++b) {
-    const int var = variant_of(r, b);
-    Chains *dst = var == 0 ? &plan->valu : var == 1 ? &plan->rb1 : &plan->rb2;
-    const long piece = piece_of[var];
+    const int kind = kind_of(r, b);
+    long L = 0;
+    for (int c = 0; c < nchunks; ++c) L += len[(size_t)c * r->B + b];
+    const long n = (L + piece - 1) / piece;
+    const long pb = n > 0 ? (long)align_up((size_t)((L + n - 1) / n), ss::kTile) : piece;
     int slot = 0;
     long filled = 0;      // tokens in the open chain
     int ranges = 0;       // items in the open chain
     auto close = [&]() {
       if (ranges == 0) return;
       dst->start.push_back((uint32_t)dst->items.size());
+      dst->kind.push_back((uint8_t)kind);
       ++slot;
       filled = 0;
       ranges = 0;
     };
     for (int c = 0; c < nchunks; ++c) {
-      const long n = len[(size_t)c * r->B + b];
+      const long nc = len[(size_t)c * r->B + b];
       long p0 = 0;
-      while (p0 < n) {
-        if (filled == piece || ranges == ss::kMaxChain) close();
+      while (p0 < nc) {
+        if (filled == pb || ranges == ss::kMaxChain) close();
         if (slot >= ss::kNumSlots) return false;
-        const long take = std::min(n - p0, piece - filled);
+        const long take = std::min(nc - p0, pb - filled);
         ss::Item it;
         it.tok_begin = (int32_t)(off[c] + p0);
         it.tok_count = (int32_t)take;
@@ -225,7 +234,7 @@ bool build_plan(const ss_round *r, int nchunks, const int32_t *len, const long p
         filled += take;
         p0 += take;
       }
-      off[c] += n;
+      off[c] += nc;
     }
     close();
     plan->slots_after[b] = std::max(plan->slots_after[b], slot);
@@ -245,38 +254,42 @@ void sort_chains(Chains *ch) {
   for (size_t c : order) {
     out.items.insert(out.items.end(), ch->items.begin() + ch->start[c], ch->items.begin() + ch->start[c + 1]);
     out.start.push_back((uint32_t)out.items.size());
+    out.kind.push_back(ch->kind[c]);
   }
   *ch = std::move(out);
 }
 
 ss_status plan_chunks(const ss_round *r, int nchunks, const int32_t *len, const std::vector<long> &tot,
                       Plan *plan) {
-  (void)tot;
-  // each kernel variant is its own launch: size its pieces from its own tokens
-  long total[3] = {0, 0, 0};
-  for (int b = 0; b < r->B; ++b)
-    for (int c = 0; c < nchunks; ++c) total[variant_of(r, b)] += len[(size_t)c * r->B + b];
-  const long pmax = max_piece_tokens(r);
-  long piece[3];
-  for (int v = 0; v < 3; ++v) {
-    if (r->split_tokens > 0) {
-      piece[v] = r->split_tokens;
-    } else {
-      const long work = total[v] * r->Hkv;
-      piece[v] = (work + kTargetWorkgroups - 1) / kTargetWorkgroups;
-      piece[v] = std::min<long>(kMaxAutoPiece, std::max<long>(kMinPiece, align_up(piece[v], ss::kTile)));
+  long total = 0;
+  for (long t : tot) total += t;
+  long piece;
+  if (r->split_tokens > 0) {
+    piece = r->split_tokens;
+  } else {
+    const long work = total * r->Hkv;
+    piece = (work + kTargetWorkgroups - 1) / kTargetWorkgroups;
+    // Ragged requests make units of unequal size; the longest-first order
+    // then needs several units per CU to balance the tail.
+    long lmin = -1, lmax = 0;
+    for (int b = 0; b < r->B; ++b) {
+      long L = 0;
+      for (int c = 0; c < nchunks; ++c) L += len[(size_t)c * r->B + b];
+      if (L == 0) continue;
+      lmin = lmin < 0 ? L : std::min(lmin, L);
+      lmax = std::max(lmax, L);
     }
-    piece[v] = std::min(piece[v], pmax);
+    if (lmin > 0 && lmax != lmin) piece /= kRaggedSplit;
+    piece = std::min<long>(kMaxAutoPiece, std::max<long>(kMinPiece, align_up(piece, ss::kTile)));
   }
+  const long pmax = max_piece_tokens(r);
+  piece = std::min(piece, pmax);
   // every request must fit its pieces into the slots
   while (!build_plan(r, nchunks, len, piece, plan)) {
-    if (piece[0] >= pmax && piece[1] >= pmax && piece[2] >= pmax)
-      return fail(SS_ERR_INVALID_ARGUMENT, "too many tokens per request for one history call");
-    for (int v = 0; v < 3; ++v) piece[v] = std::min(pmax, piece[v] * 2);
+    if (piece >= pmax) return fail(SS_ERR_INVALID_ARGUMENT, "too many tokens per request for one history call");
+    piece = std::min(pmax, piece * 2);
   }
-  sort_chains(&plan->valu);
-  sort_chains(&plan->rb1);
-  sort_chains(&plan->rb2);
+  sort_chains(&plan->chains);
   return SS_OK;
 }
 
@@ -313,7 +326,7 @@ hipError_t launch_units(ss::ChunkParams *p, const Chains &ch, F launch) {
     const uint32_t i0 = ch.start[c0], n = ch.start[c1] - i0;
     std::memcpy(p->items, ch.items.data() + i0, n * sizeof(ss::Item));
     for (size_t c = c0; c < c1; ++c)
-      p->units[c - c0] = (ch.start[c] - i0) | ((ch.start[c + 1] - ch.start[c]) << 16);
+      p->units[c - c0] = (ch.start[c] - i0) | ((ch.start[c + 1] - ch.start[c]) << 16) | ((uint32_t)ch.kind[c] << 24);
     p->num_items = (int32_t)n;
     p->num_units = (int32_t)(c1 - c0);
     const hipError_t e = launch(*p);
@@ -345,11 +358,7 @@ ss_status enqueue_history(ss_round *r, int nchunks, const void *const *k, const 
   ss_status s = plan_chunks(r, nchunks, len, tot, &plan);
   if (s != SS_OK) return s;
   ss::ChunkParams *p = base_params(r, nchunks, k, v, tot);
-  hipError_t e = launch_units(p, plan.rb2, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 2, stream); });
-  if (e == hipSuccess)
-    e = launch_units(p, plan.rb1, [&](const ss::ChunkParams &q) { return ss::launch_chunk_mfma(q, 1, stream); });
-  if (e == hipSuccess)
-    e = launch_units(p, plan.valu, [&](const ss::ChunkParams &q) { return ss::launch_chunk_valu(q, stream); });
+  const hipError_t e = launch_units(p, plan.chains, [&](const ss::ChunkParams &q) { return ss::launch_chunk(q, stream); });
   if (e != hipSuccess) return hip_fail(e, "history chunk kernel launch");
   r->slots_used = plan.slots_after;   // the slots written by this call are valid from now on
   return SS_OK;

@@ -18,6 +18,12 @@ constexpr int kMaxCand = 8;         // candidates per request (k_b + 1)
 constexpr int kMaxValuRows = 4;     // rows per KV head the VALU chunk kernel handles
 constexpr int kMaxRows = 32;        // rows per KV head the MFMA chunk kernel handles
 
+// Unit kinds: the chunk kernel body that attends a unit (rows per KV head
+// M = n_b * G: <= 4 on the VALU path, else MFMA with ceil(M / 16) blocks).
+constexpr int kUnitValu = 0;
+constexpr int kUnitMfma1 = 1;
+constexpr int kUnitMfma2 = 2;
+
 // Item flag: the slot has not been written in this round yet, so the kernel
 // stores its result instead of merging with (uninitialised) workspace.
 constexpr int kSlotFresh = 1;
@@ -65,7 +71,8 @@ struct ChunkParams {
   const uint16_t *v[kMaxChunks];
   uint64_t head_stride[kMaxChunks];   // elements between KV heads at the same token
   int32_t num_units;
-  // unit u = items [units[u] & 0xffff, + (units[u] >> 16)), 1..kMaxChain items
+  // unit u = items [units[u] & 0xffff, + ((units[u] >> 16) & 0xff)), 1..kMaxChain
+  // items, attended by the body units[u] >> 24 (kUnitValu / kUnitMfma1 / kUnitMfma2)
   uint32_t units[kMaxUnits];
   Item items[kMaxItems];
 };
@@ -84,8 +91,8 @@ struct FinalParams {
 };
 
 // Launch wrappers; return hipGetLastError() of the launch.
-hipError_t launch_chunk_mfma(const ChunkParams &p, int row_blocks, hipStream_t s);
-hipError_t launch_chunk_valu(const ChunkParams &p, hipStream_t s);
+// History units of every kind, grid (num_units, Hkv).
+hipError_t launch_chunk(const ChunkParams &p, hipStream_t s);
 // Speculative Frontier pass fused with the split-slot merge and O = a / l.
 hipError_t launch_finalize(const FinalParams &p, hipStream_t s);
 

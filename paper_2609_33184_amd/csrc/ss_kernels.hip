@@ -151,7 +151,7 @@ __device__ __forceinline__ void fold_into_slot(const ChunkParams &p, const Item 
 }
 
 // ---------------------------------------------------------------------------
-// MFMA chunk kernel.  Workgroup = (unit, kv head); 4 waves; wave w takes the
+// MFMA chunk body.  Workgroup = (unit, kv head); 4 waves; wave w takes the
 // 32-token tiles w, w+4, ... of the unit's chain of items (one request's
 // token ranges, possibly from several chunks, attended as one sequence).
 // Per tile:
@@ -240,15 +240,11 @@ __device__ __forceinline__ s16x4_t lds_read_tr16(const unsigned char *p) {
 }
 
 template <int RB>
-__global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[MfmaLds<RB>::kBytes];
+__device__ __forceinline__ void mfma_unit(const ChunkParams &p, unsigned char *smem, int i0, int nit) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15;
   const int lq = lane >> 4;
-  const uint32_t unit = p.units[blockIdx.x];
-  const int i0 = unit & 0xffff;
-  const int nit = unit >> 16;
   const Item it = p.items[i0];          // request, slot and flags of the whole chain
   const int g = blockIdx.y;
   const int M = it.n_cand * p.G;
@@ -466,22 +462,18 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_mfma(const ChunkParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// VALU chunk kernel for sparse query groups (few rows per KV head): fp32 dot
+// VALU chunk body for sparse query groups (few rows per KV head): fp32 dot
 // products on the vector ALUs, exact fp32 softmax weights.  Lane l: d-chunk
 // c = l % 16 (8 values), token group tg = l / 16; a 32-token tile is 8
 // coalesced loads (4 token rows of 256 B each) of K and of V.  Scores are
 // reduced over the 16 lanes of a DPP row.
 // ---------------------------------------------------------------------------
 template <int MAXR>
-__global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
-  __shared__ __attribute__((aligned(16))) float smem[kWaves * MAXR * (kAwPitch + 2)];
+__device__ __forceinline__ void valu_unit(const ChunkParams &p, float *smem, int i0, int nit) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int lane = threadIdx.x & 63;
   const int c = lane & 15;
   const int tg = lane >> 4;
-  const uint32_t unit = p.units[blockIdx.x];
-  const int i0 = unit & 0xffff;
-  const int nit = unit >> 16;
   const Item it = p.items[i0];          // request, slot and flags of the whole chain
   const int g = blockIdx.y;
   const int M = it.n_cand * p.G;
@@ -645,6 +637,31 @@ __global__ void __launch_bounds__(256, 2) chunk_attn_valu(const ChunkParams p) {
   fold_into_slot<MAXR>(p, it, g, M, aw, mw, lw);
 }
 
+constexpr int kValuLdsBytes = kWaves * kMaxValuRows * (kAwPitch + 2) * 4;
+constexpr int kChunkLdsBytes = MfmaLds<2>::kBytes > kValuLdsBytes ? MfmaLds<2>::kBytes : kValuLdsBytes;
+static_assert(MfmaLds<1>::kBytes <= kChunkLdsBytes, "LDS sizes");
+
+// ---------------------------------------------------------------------------
+// History kernel: one launch for every unit of a call.  Workgroup =
+// (unit, kv head); the unit's kind (from the unit table) selects the body:
+// MFMA with two or one 16-row blocks, or the VALU path for <= 4 rows.  One
+// launch keeps the whole call in a single wave of workgroups whatever the
+// mix of candidate counts in the Cohort.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256, 2) chunk_attn(const ChunkParams p) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kChunkLdsBytes];
+  const uint32_t unit = p.units[blockIdx.x];
+  const int i0 = unit & 0xffff;
+  const int nit = (unit >> 16) & 0xff;
+  const int kind = unit >> 24;
+  if (kind == kUnitMfma2)
+    mfma_unit<2>(p, smem, i0, nit);
+  else if (kind == kUnitMfma1)
+    mfma_unit<1>(p, smem, i0, nit);
+  else
+    valu_unit<kMaxValuRows>(p, reinterpret_cast<float *>(smem), i0, nit);
+}
+
 // ---------------------------------------------------------------------------
 // Finalize: for every query row (request b, candidate i, head h)
 //   * attend the Speculative Frontier: candidate keys j <= i of the same
@@ -755,17 +772,8 @@ __global__ void __launch_bounds__(256) finalize_kernel(const FinalParams p) {
 
 }  // namespace
 
-hipError_t launch_chunk_mfma(const ChunkParams &p, int row_blocks, hipStream_t s) {
-  const dim3 grid(p.num_units, p.Hkv);
-  if (row_blocks == 1)
-    hipLaunchKernelGGL(chunk_attn_mfma<1>, grid, dim3(256), 0, s, p);
-  else
-    hipLaunchKernelGGL(chunk_attn_mfma<2>, grid, dim3(256), 0, s, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_chunk_valu(const ChunkParams &p, hipStream_t s) {
-  hipLaunchKernelGGL(chunk_attn_valu<kMaxValuRows>, dim3(p.num_units, p.Hkv), dim3(256), 0, s, p);
+hipError_t launch_chunk(const ChunkParams &p, hipStream_t s) {
+  hipLaunchKernelGGL(chunk_attn, dim3(p.num_units, p.Hkv), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

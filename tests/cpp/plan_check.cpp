@@ -29,8 +29,7 @@ static void rec(const ChunkParams &p, int kind) {
   g_recs.push_back(r);
   g_last = &p;
 }
-hipError_t launch_chunk_mfma(const ChunkParams &p, int rb, hipStream_t) { rec(p, rb); return hipSuccess; }
-hipError_t launch_chunk_valu(const ChunkParams &p, hipStream_t) { rec(p, 0); return hipSuccess; }
+hipError_t launch_chunk(const ChunkParams &p, hipStream_t) { rec(p, -1); return hipSuccess; }
 hipError_t launch_finalize(const FinalParams &, hipStream_t) { return hipSuccess; }
 }
 
@@ -62,7 +61,7 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
   for (int b = 1; b < B; ++b) off_rows[b] = off_rows[b - 1] + ncand[b - 1];
   for (auto &rc : g_recs) {
     for (size_t u = 0; u < rc.units.size(); ++u) {
-      const int i0 = rc.units[u] & 0xffff, nit = rc.units[u] >> 16;
+      const int i0 = rc.units[u] & 0xffff, nit = (rc.units[u] >> 16) & 0xff, kind = rc.units[u] >> 24;
       CHECK(nit >= 1 && nit <= ss::kMaxChain && i0 + nit <= (int)rc.items.size(), "unit table");
       const ss::Item &it = rc.items[i0];
       int b = -1;
@@ -70,7 +69,7 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
       CHECK(b >= 0, "q_row0");
       const int M = it.n_cand * G;
       const int want_kind = (M < (mfma_min_rows ? mfma_min_rows : 5) && M <= 4) ? 0 : (M <= 16 ? 1 : 2);
-      CHECK(rc.kind == want_kind, "kernel kind %d want %d (M=%d)", rc.kind, want_kind, M);
+      CHECK(kind == want_kind, "unit kind %d want %d (M=%d)", kind, want_kind, M);
       int ntiles = 0;
       long toks = 0;
       for (int k = 0; k < nit; ++k) {
