@@ -38,7 +38,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 METRIC = "verify-attention effective KV GB/s (% of HBM peak) + round latency @32K ctx"
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_33184_amd", "csrc", "ss_kernels.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "chunk_attn_mfma_config3_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "chunk_attn_config3_traffic.json")
 
 
 def kernel_source_hash() -> str:
@@ -476,7 +476,7 @@ def main() -> int:
             "wall_s_timed": round(wall, 4),
         },
         "roofline": {
-            "kernel": f"chunk_attn_mfma<2> (history launch over {batch} chunk(s))",
+            "kernel": f"chunk_attn (history kernel, two-block MFMA units; one launch over {batch} chunk(s))",
             "bound": "hbm",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,

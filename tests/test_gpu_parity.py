@@ -116,6 +116,24 @@ def test_config5_one_layer_full_size(stream):
     check_sampled(w, b.out, b.lse, [(0, 1), (31, 6)], what="config5 layer0")
 
 
+def test_batched_calls_small_and_full_depth(stream):
+    """Configs 1, 2 and 5 with every chunk in one ss_attend_history_chunks
+    call (the launch configuration the benchmark's per-config table times)."""
+    for cfg in (1, 2):
+        w = W.workload(cfg)
+        print(f"config {cfg}, one batched history call over {w.num_chunks} chunks", flush=True)
+        b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR, batch=w.num_chunks)
+        _full_check(w, b, f"config{cfg} batched")
+    w = W.workload(5)
+    print("config 5, layer 17, one batched history call over 16 chunks", flush=True)
+    b = H.RoundBuffers(w, layer=17, kv_layout=ss.SS_KV_HEAD_MAJOR)
+    chunks = H.hbm_history(w, kv_layout=ss.SS_KV_HEAD_MAJOR)
+    torch.cuda.synchronize()
+    H.run_round(b, chunks, stream.cuda_stream, batch=w.num_chunks)
+    stream.synchronize()
+    check_sampled(w, b.out, b.lse, [(5, 0), (20, 4)], layer=17, what="config5 batched layer17")
+
+
 def test_small_edge_cases(stream):
     cases = [
         ([0], [1], 8, 2),                # empty history, decode
