@@ -237,33 +237,61 @@ def config_table(torch, H, ss, W, stream, layout: int, rounds: int):
     return table
 
 
-def full_depth_streamed(torch, H, ss, W, stream, layout: int, layers: int):
+def full_depth_streamed(torch, H, ss, W, stream, layout: int, layers: int, batch: int = 1):
     """Config 5 end to end: `layers` layers (each its own queries) whose
     shared 16 GiB history streams from pinned host memory through one
-    continuous two-slot pipeline."""
+    continuous two-slot pipeline (transfer batches of `batch` chunks), timed
+    without and with a stand-in for the rest of each layer (output projection
+    and feed-forward GEMMs of a 4096-wide, 14336-FFN model over the round's
+    256 query tokens) between the layers' attention, which the next layer's
+    uploads run ahead of."""
     w = W.workload(5)
     log(f"bench: full-depth streamed round, {layers} layers: filling pinned host history")
     host = H.HostHistory(w, kv_layout=layout)
-    pipe = H.Pipeline(host.max_chunk_bytes())
+    pipe = H.Pipeline(H.batch_bytes(host, batch))
+    g = torch.Generator(device="cuda").manual_seed(5)
+    x = torch.randn(w.total_rows, 4096, device="cuda", dtype=torch.bfloat16, generator=g)
+    wo = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16, generator=g) * 0.01
+    w13 = torch.randn(4096, 2 * 14336, device="cuda", dtype=torch.bfloat16, generator=g) * 0.01
+    w2 = torch.randn(14336, 4096, device="cuda", dtype=torch.bfloat16, generator=g) * 0.01
+
+    def rest_of_layer():
+        with torch.cuda.stream(stream):
+            h = (x @ wo) @ w13
+            _ = h[:, :14336] @ w2
+
+    res = {"workload": w.name, "layers": layers, "transfer_batch_chunks": batch}
     try:
         bufs = [H.RoundBuffers(w, layer=l, kv_layout=layout) for l in range(layers)]
         torch.cuda.synchronize()
-        H.run_round_streamed(bufs[0], host, pipe, stream.cuda_stream)     # warm-up layer
+        H.run_round_streamed(bufs[0], host, pipe, stream.cuda_stream, batch=batch)     # warm-up layer
+        rest_of_layer()
         torch.cuda.synchronize()
+        for with_gemm in (False, True):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for b in bufs:
+                H.run_round_streamed(b, host, pipe, stream.cuda_stream, batch=batch)
+                if with_gemm:
+                    rest_of_layer()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            t = e0.elapsed_time(e1) / 1e3
+            key = "with_layer_gemms" if with_gemm else "attention_only"
+            res[key] = {"round_s": round(t, 4), "per_layer_ms": round(t / layers * 1e3, 3),
+                        "host_link_GBs": round(host.total_bytes * layers / t / 1e9, 2)}
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        for b in bufs:
-            H.run_round_streamed(b, host, pipe, stream.cuda_stream)
+        rest_of_layer()
         e1.record(stream)
         torch.cuda.synchronize()
-        t = e0.elapsed_time(e1) / 1e3
+        res["layer_gemms_alone_ms"] = round(e0.elapsed_time(e1), 4)
     finally:
         pipe.close()
-    h2d = host.total_bytes * layers
-    return {"workload": w.name, "layers": layers, "round_s": round(t, 4), "per_layer_ms": round(t / layers * 1e3, 3),
-            "h2d_bytes": h2d, "host_link_GBs": round(h2d / t / 1e9, 2),
-            "in_hbm_equivalent_KV_GBs": round(w.algorithmic_kv_bytes() * layers / t / 1e9, 2)}
+    res["h2d_bytes"] = host.total_bytes * layers
+    return res
 
 
 def ablation(torch, H, ss, W, stream, layout: int):
@@ -372,6 +400,8 @@ def main() -> int:
                     help="skip the in-HBM rounds of the other configurations")
     ap.add_argument("--full-depth", type=int, default=0, metavar="LAYERS",
                     help="also time config 5 end to end: LAYERS layers streamed through one pipeline")
+    ap.add_argument("--transfer-batch", type=int, default=1,
+                    help="chunks per transfer batch in the full-depth streamed round")
     ap.add_argument("--ablation", action="store_true",
                     help="also run the K1/K2/K3 (restore / stream / stream+prefetch) comparison")
     args = ap.parse_args()
@@ -510,7 +540,8 @@ def main() -> int:
         torch.cuda.empty_cache()
         out["other_configs_in_hbm"] = config_table(torch, H, ss, W, stream, layout, max(5, args.steps // 2))
     if args.full_depth > 0:
-        out["full_depth_streamed"] = full_depth_streamed(torch, H, ss, W, stream, layout, args.full_depth)
+        out["full_depth_streamed"] = full_depth_streamed(torch, H, ss, W, stream, layout, args.full_depth,
+                                                         args.transfer_batch)
     if args.ablation:
         out["ablation_k1_k2_k3"] = ablation(torch, H, ss, W, stream, layout)
     print(json.dumps(out), flush=True)

@@ -187,6 +187,16 @@ ss_status ss_pipeline_create(ss_pipeline **out, void *staging0, void *staging1, 
 ss_status ss_pipeline_attend_chunk(ss_pipeline *p, ss_round *r, const void *host_kv,
                                    const int32_t *len, hipStream_t stream);
 
+/* Transfer batch (paper Sec. 4.2: adjacent chunks are grouped into transfer
+ * batches to amortise copy submission, synchronisation and kernel launches):
+ * upload num_chunks adjacent history chunks into the next staging slot with
+ * one copy and attend them with one launch, as ss_attend_history_chunks
+ * does.  host_kv: pinned host memory holding chunk 0's K, chunk 0's V, chunk
+ * 1's K, ... contiguously (each in the round's kv_layout); len: host
+ * [num_chunks][B]; 1 <= num_chunks <= 32; the batch must fit slot_bytes. */
+ss_status ss_pipeline_attend_chunks(ss_pipeline *p, ss_round *r, int32_t num_chunks, const void *host_kv,
+                                    const int32_t *len, hipStream_t stream);
+
 /* Destroy the pipeline's events (after its work has completed). */
 void ss_pipeline_destroy(ss_pipeline *p);
 

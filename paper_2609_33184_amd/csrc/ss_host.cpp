@@ -556,30 +556,45 @@ ss_status ss_pipeline_create(ss_pipeline **out, void *staging0, void *staging1, 
   return SS_OK;
 }
 
-ss_status ss_pipeline_attend_chunk(ss_pipeline *p, ss_round *r, const void *host_kv, const int32_t *len,
-                                   hipStream_t stream) {
+ss_status ss_pipeline_attend_chunks(ss_pipeline *p, ss_round *r, int32_t num_chunks, const void *host_kv,
+                                    const int32_t *len, hipStream_t stream) {
   if (p == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "pipeline is null");
-  std::vector<long> tot;
+  ss_status s = check_round(r);
+  if (s != SS_OK) return s;
+  if (num_chunks < 1 || num_chunks > ss::kMaxChunks)
+    return fail(SS_ERR_INVALID_ARGUMENT, "num_chunks = %d outside [1, %d]", num_chunks, ss::kMaxChunks);
+  if (len == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "len is null");
+  // chunk c occupies [off[c], off[c] + 2 * half[c]) of the slot: its K, then its V
   const int sl = p->next;
-  long total = 0;
-  if (len != nullptr && r != nullptr)
-    for (int b = 0; b < r->B; ++b) total += std::max<int32_t>(0, len[b]);
-  const size_t half = r != nullptr ? (size_t)total * r->Hkv * ss::kHeadDim * 2 : 0;
-  const void *kk[1] = {p->slot[sl]};
-  const void *vv[1] = {p->slot[sl] + half};
-  ss_status s = check_history_args(r, 1, kk, vv, len, &tot);
+  std::vector<const void *> kk(num_chunks), vv(num_chunks);
+  size_t bytes = 0;
+  for (int c = 0; c < num_chunks; ++c) {
+    long total = 0;
+    for (int b = 0; b < r->B; ++b) total += std::max<int32_t>(0, len[(size_t)c * r->B + b]);
+    const size_t half = (size_t)total * r->Hkv * ss::kHeadDim * 2;
+    kk[c] = p->slot[sl] + bytes;
+    vv[c] = p->slot[sl] + bytes + half;
+    bytes += 2 * half;
+  }
+  std::vector<long> tot;
+  s = check_history_args(r, num_chunks, kk.data(), vv.data(), len, &tot);
   if (s != SS_OK) return s;
-  if (total == 0) return SS_OK;
+  if (bytes == 0) return SS_OK;
   if (host_kv == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "host_kv is null");
-  if (2 * half > p->slot_bytes)
-    return fail(SS_ERR_INVALID_ARGUMENT, "chunk needs %zu bytes > slot_bytes %zu", 2 * half, p->slot_bytes);
-  s = ss_upload_chunk(p->slot[sl], host_kv, 2 * half, p->copy, p->used[sl] ? p->freed[sl] : nullptr, p->ready[sl]);
+  if (bytes > p->slot_bytes)
+    return fail(SS_ERR_INVALID_ARGUMENT, "chunks need %zu bytes > slot_bytes %zu", bytes, p->slot_bytes);
+  s = ss_upload_chunk(p->slot[sl], host_kv, bytes, p->copy, p->used[sl] ? p->freed[sl] : nullptr, p->ready[sl]);
   if (s != SS_OK) return s;
-  s = attend_history(r, 1, kk, vv, len, p->ready[sl], p->freed[sl], stream);
+  s = attend_history(r, num_chunks, kk.data(), vv.data(), len, p->ready[sl], p->freed[sl], stream);
   if (s != SS_OK) return s;
   p->used[sl] = true;
   p->next = sl ^ 1;
   return SS_OK;
+}
+
+ss_status ss_pipeline_attend_chunk(ss_pipeline *p, ss_round *r, const void *host_kv, const int32_t *len,
+                                   hipStream_t stream) {
+  return ss_pipeline_attend_chunks(p, r, 1, host_kv, len, stream);
 }
 
 void ss_pipeline_destroy(ss_pipeline *p) {

@@ -142,14 +142,29 @@ class Pipeline:
             self.handle = None
 
 
+def batch_bytes(host: HostHistory, batch: int) -> int:
+    """Largest staging slot a transfer batch of `batch` adjacent chunks needs."""
+    n = len(host.sizes)
+    return max([sum(host.sizes[j:j + batch]) for j in range(0, n, batch)] or [0])
+
+
 def run_round_streamed(b: RoundBuffers, host: HostHistory, pipe: Pipeline, stream: int,
-                       order: Optional[Sequence[int]] = None) -> None:
-    """Enqueue one round whose history streams from pinned host memory."""
+                       order: Optional[Sequence[int]] = None, batch: int = 1) -> None:
+    """Enqueue one round whose history streams from pinned host memory; with
+    ``batch`` > 1, groups of that many adjacent chunks travel as one transfer
+    batch (one copy, one attention launch)."""
     w = b.w
+    if batch > 1 and order is not None:
+        raise ValueError("transfer batches take the chunks in their host order")
     order = list(range(w.num_chunks)) if order is None else list(order)
     r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream)
     try:
-        for j in order:
+        if batch > 1:
+            for j0 in range(0, w.num_chunks, batch):
+                grp = range(j0, min(w.num_chunks, j0 + batch))
+                ss.ss_pipeline_attend_chunks(pipe.handle, r, host.chunk_ptr(j0), [w.chunk_lens(j) for j in grp],
+                                             stream)
+        for j in (order if batch <= 1 else []):
             ss.ss_pipeline_attend_chunk(pipe.handle, r, host.chunk_ptr(j), w.chunk_lens(j), stream)
         ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
         ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream)

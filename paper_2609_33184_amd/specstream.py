@@ -31,7 +31,7 @@ EXPORTED = (
     "ss_round_workspace_bytes", "ss_round_init", "ss_upload_chunk", "ss_attend_history_chunk",
     "ss_attend_history_chunks",
     "ss_attend_local_candidates", "ss_round_finalize", "ss_round_destroy", "ss_pipeline_create",
-    "ss_pipeline_attend_chunk", "ss_pipeline_destroy", "ss_event_create", "ss_event_destroy",
+    "ss_pipeline_attend_chunk", "ss_pipeline_attend_chunks", "ss_pipeline_destroy", "ss_event_create", "ss_event_destroy",
     "ss_status_string", "ss_last_error",
 )
 
@@ -96,6 +96,7 @@ def load() -> ctypes.CDLL:
         "ss_round_destroy": (None, [P]),
         "ss_pipeline_create": (I32, [ctypes.POINTER(P), P, P, SZ, P]),
         "ss_pipeline_attend_chunk": (I32, [P, P, P, PI32, P]),
+        "ss_pipeline_attend_chunks": (I32, [P, P, I32, P, PI32, P]),
         "ss_pipeline_destroy": (None, [P]),
         "ss_event_create": (I32, [ctypes.POINTER(P)]),
         "ss_event_destroy": (None, [P]),
@@ -185,6 +186,12 @@ def ss_pipeline_create(staging0: int, staging1: int, slot_bytes: int, copy_strea
 
 def ss_pipeline_attend_chunk(p: int, r: int, host_kv: int, len_: Sequence[int], stream: int = 0) -> None:
     _check(load().ss_pipeline_attend_chunk(p, r, host_kv, _lens(len_), stream), "ss_pipeline_attend_chunk")
+
+
+def ss_pipeline_attend_chunks(p: int, r: int, host_kv: int, lens: Sequence[Sequence[int]], stream: int = 0) -> None:
+    flat = [int(x) for row in lens for x in row]
+    _check(load().ss_pipeline_attend_chunks(p, r, len(lens), host_kv, (ctypes.c_int32 * len(flat))(*flat), stream),
+           "ss_pipeline_attend_chunks")
 
 
 def ss_pipeline_destroy(p: Optional[int]) -> None:

@@ -142,6 +142,19 @@ def test_call_order_and_chunk_arguments(lib):
     assert e.value.status == ss.SS_ERR_INVALID_ARGUMENT
 
 
+def test_pipeline_argument_checks(lib):
+    d = ss.make_desc([2], 8, 2, max_chunk_tokens=1024)
+    r = ss.ss_round_init(d, FAKE_Q, FAKE_WS, ss.ss_round_workspace_bytes(d))
+    try:
+        for call in (lambda: ss.ss_pipeline_attend_chunks(None, r, FAKE_Q, [[16]]),
+                     lambda: ss.ss_pipeline_attend_chunk(None, r, FAKE_Q, [16])):
+            with pytest.raises(ss.SpecStreamError) as e:
+                call()
+            assert e.value.status == ss.SS_ERR_INVALID_ARGUMENT
+    finally:
+        ss.ss_round_destroy(r)
+
+
 def test_upload_argument_checks(lib):
     with pytest.raises(ss.SpecStreamError) as e:
         ss.ss_upload_chunk(0, FAKE_Q, 16)

@@ -138,6 +138,30 @@ def test_streamed_equals_in_hbm(stream, layout):
             pipe.close()
 
 
+def test_transfer_batches_equal_in_hbm_batches(stream):
+    """Streaming groups of adjacent chunks as transfer batches (one copy, one
+    launch each) gives bitwise the in-HBM result with the same grouping."""
+    w = W.custom([5000, 123, 4096, 2500], [3, 8, 1, 6], num_q_heads=32, num_kv_heads=8, chunk_tokens=1024,
+                 seed_base=16)
+    layout = ss.SS_KV_HEAD_MAJOR
+    host = H.HostHistory(w, kv_layout=layout)
+    for batch in (2, 3, w.num_chunks):
+        print(f"transfer batches of {batch} chunks", flush=True)
+        b, _ = _round(w, stream, kv_layout=layout, batch=batch)
+        ref = b.out.clone()
+        pipe = H.Pipeline(H.batch_bytes(host, batch))
+        try:
+            b2 = H.RoundBuffers(w, kv_layout=layout)
+            torch.cuda.synchronize()
+            H.run_round_streamed(b2, host, pipe, stream.cuda_stream, batch=batch)
+            stream.synchronize()
+            assert torch.equal(b2.out, ref), batch
+        finally:
+            pipe.close()
+    ref_o, _ = oracle_full(w)
+    assert_parity(ref.double().cpu().numpy(), ref_o, "transfer batches")
+
+
 def test_pipeline_poison_and_delay(stream):
     """A staging slot overwritten with NaNs right after its free event, and
     uploads delayed behind long copy-stream work, change nothing."""
