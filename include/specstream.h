@@ -200,6 +200,59 @@ ss_status ss_pipeline_attend_chunks(ss_pipeline *p, ss_round *r, int32_t num_chu
 /* Destroy the pipeline's events (after its work has completed). */
 void ss_pipeline_destroy(ss_pipeline *p);
 
+/* ---- Commit-aware KV tiering (paper Sec. 4.1) ------------------------------
+ * Per request the Target KV is split at 0 <= H <= C <= L (Eq. 8):
+ *   [0, H)  Sealed History       host (pinned memory), streamed as chunks
+ *   [H, C)  Active Tail          GPU, committed tokens not yet migrated
+ *   [C, L)  Speculative Frontier GPU, candidates awaiting verification
+ * Committed tokens older than the tail target T move to the host in blocks
+ * of g tokens; H advances only after the copy has completed, and the
+ * rejected suffix of the frontier is released on the GPU alone (it never
+ * overlaps [0, H), so no host cleanup or cross-device rollback exists). */
+
+/* Eq. 9: end of the next migration, E = max(H, g * floor(max(0, C - T) / g)).
+ * Requires H >= 0, C >= H, T >= 0, g >= 1 and H a multiple of g; returns -1
+ * otherwise.  E == H means nothing to migrate. */
+int64_t ss_tier_endpoint(int64_t H, int64_t C, int64_t T, int64_t g);
+
+typedef struct ss_tier ss_tier;   /* opaque host-side boundaries of a Cohort */
+
+/* New tiering state for num_requests requests, all boundaries 0; tail_target
+ * = T >= 0 tokens kept on the GPU, granularity = g >= 1 tokens per migration
+ * block.  Host memory only; free with ss_tier_destroy. */
+ss_status ss_tier_create(ss_tier **out, int32_t num_requests, int64_t tail_target, int64_t granularity);
+void ss_tier_destroy(ss_tier *t);
+
+/* Boundaries of request b (each pointer nullable). */
+ss_status ss_tier_get(const ss_tier *t, int32_t b, int64_t *H, int64_t *C, int64_t *L);
+
+/* n >= 0 new tokens enter the frontier (the round's candidates, or a
+ * prompt before its commit): L += n. */
+ss_status ss_tier_extend(ss_tier *t, int32_t b, int64_t n);
+
+/* Verification kept the first `accepted` frontier tokens (0 <= accepted <=
+ * L - C): C' = C + accepted; the suffix [C', L) is released (its range is
+ * returned through the nullable released_* pointers) and L = C'. */
+ss_status ss_tier_commit(ss_tier *t, int32_t b, int64_t accepted, int64_t *released_begin,
+                         int64_t *released_end);
+
+/* Plan request b's next migration (Eq. 9).  If none is in flight and E > H,
+ * [H, E) is marked in flight and returned; otherwise begin == end.  The
+ * caller copies those tokens' K/V (ss_download_range) and calls
+ * ss_tier_complete once the copy has completed. */
+ss_status ss_tier_plan(ss_tier *t, int32_t b, int64_t *begin, int64_t *end);
+
+/* The in-flight migration of request b has completed: H = E, and the GPU
+ * space of the migrated tokens may be reclaimed.  SS_ERR_BAD_STATE if none
+ * is in flight. */
+ss_status ss_tier_complete(ss_tier *t, int32_t b);
+
+/* Device -> pinned host copy on copy_stream (a migration's copy); the same
+ * event conventions as ss_upload_chunk.  dst must be page-locked host memory
+ * (else SS_ERR_NOT_PINNED), src device memory; bytes > 0. */
+ss_status ss_download_range(void *dst_pinned_host, const void *src_device, size_t bytes,
+                            hipStream_t copy_stream, hipEvent_t wait_before, hipEvent_t signal_after);
+
 /* Event helpers so callers need no HIP binding of their own.  Events are
  * created with timing disabled. */
 ss_status ss_event_create(hipEvent_t *e);

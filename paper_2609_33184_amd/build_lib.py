@@ -34,9 +34,11 @@ def build(verbose: bool = True) -> str:
     kobj = os.path.join(bdir, "ss_kernels.o")
     _run([HIPCC, *COMMON, *DEVICE_ONLY, "-c", os.path.join(CSRC, "ss_kernels.hip"), "-o", kobj])
     objs.append(kobj)
-    hobj = os.path.join(bdir, "ss_host.o")
-    _run([HIPCC, *COMMON, "-x", "c++", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", "-c", os.path.join(CSRC, "ss_host.cpp"), "-o", hobj])
-    objs.append(hobj)
+    for name in ("ss_host", "ss_tier"):
+        hobj = os.path.join(bdir, name + ".o")
+        _run([HIPCC, *COMMON, "-x", "c++", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", "-c",
+              os.path.join(CSRC, name + ".cpp"), "-o", hobj])
+        objs.append(hobj)
     tmp = LIB + ".tmp"
     _run([HIPCC, *DEVICE_ONLY, "-shared", "-fPIC", *objs, "-o", tmp])
     shutil.move(tmp, LIB)

@@ -12,11 +12,14 @@
 #include <string>
 #include <vector>
 
+#include "ss_error.h"
 #include "ss_kernels.h"
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
+
+namespace ss {
 
 ss_status fail(ss_status s, const char *fmt, ...) {
   char buf[512];
@@ -31,6 +34,13 @@ ss_status fail(ss_status s, const char *fmt, ...) {
 ss_status hip_fail(hipError_t e, const char *what) {
   return fail(SS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
+
+}  // namespace ss
+
+namespace {
+
+using ss::fail;
+using ss::hip_fail;
 
 inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }

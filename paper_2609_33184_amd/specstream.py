@@ -33,6 +33,8 @@ EXPORTED = (
     "ss_attend_local_candidates", "ss_round_finalize", "ss_round_destroy", "ss_pipeline_create",
     "ss_pipeline_attend_chunk", "ss_pipeline_attend_chunks", "ss_pipeline_destroy", "ss_event_create", "ss_event_destroy",
     "ss_status_string", "ss_last_error",
+    "ss_tier_endpoint", "ss_tier_create", "ss_tier_destroy", "ss_tier_get", "ss_tier_extend", "ss_tier_commit",
+    "ss_tier_plan", "ss_tier_complete", "ss_download_range",
 )
 
 
@@ -85,6 +87,7 @@ def load() -> ctypes.CDLL:
     lib = ctypes.CDLL(_LIB_PATH)
     P, I32, SZ, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t, ctypes.POINTER(ctypes.c_float)
     PI32 = ctypes.POINTER(ctypes.c_int32)
+    I64, PI64 = ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)
     sig = {
         "ss_round_workspace_bytes": (SZ, [ctypes.POINTER(ss_round_desc)]),
         "ss_round_init": (I32, [ctypes.POINTER(P), ctypes.POINTER(ss_round_desc), P, P, SZ, P]),
@@ -102,6 +105,15 @@ def load() -> ctypes.CDLL:
         "ss_event_destroy": (None, [P]),
         "ss_status_string": (ctypes.c_char_p, [I32]),
         "ss_last_error": (ctypes.c_char_p, []),
+        "ss_tier_endpoint": (I64, [I64, I64, I64, I64]),
+        "ss_tier_create": (I32, [ctypes.POINTER(P), I32, I64, I64]),
+        "ss_tier_destroy": (None, [P]),
+        "ss_tier_get": (I32, [P, I32, PI64, PI64, PI64]),
+        "ss_tier_extend": (I32, [P, I32, I64]),
+        "ss_tier_commit": (I32, [P, I32, I64, PI64, PI64]),
+        "ss_tier_plan": (I32, [P, I32, PI64, PI64]),
+        "ss_tier_complete": (I32, [P, I32]),
+        "ss_download_range": (I32, [P, P, SZ, P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -206,3 +218,52 @@ def ss_event_create() -> int:
 
 def ss_event_destroy(e: Optional[int]) -> None:
     load().ss_event_destroy(e)
+
+
+# ---------------------------------------------------------------------------
+# commit-aware tiering (paper Sec. 4.1)
+# ---------------------------------------------------------------------------
+def ss_tier_endpoint(H: int, C: int, T: int, g: int) -> int:
+    return int(load().ss_tier_endpoint(H, C, T, g))
+
+
+def ss_tier_create(num_requests: int, tail_target: int, granularity: int) -> int:
+    h = ctypes.c_void_p()
+    _check(load().ss_tier_create(ctypes.byref(h), num_requests, tail_target, granularity), "ss_tier_create")
+    return h.value
+
+
+def ss_tier_destroy(t: Optional[int]) -> None:
+    load().ss_tier_destroy(t)
+
+
+def ss_tier_get(t: int, b: int):
+    H, C, L = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(load().ss_tier_get(t, b, ctypes.byref(H), ctypes.byref(C), ctypes.byref(L)), "ss_tier_get")
+    return H.value, C.value, L.value
+
+
+def ss_tier_extend(t: int, b: int, n: int) -> None:
+    _check(load().ss_tier_extend(t, b, n), "ss_tier_extend")
+
+
+def ss_tier_commit(t: int, b: int, accepted: int):
+    lo, hi = ctypes.c_int64(), ctypes.c_int64()
+    _check(load().ss_tier_commit(t, b, accepted, ctypes.byref(lo), ctypes.byref(hi)), "ss_tier_commit")
+    return lo.value, hi.value
+
+
+def ss_tier_plan(t: int, b: int):
+    lo, hi = ctypes.c_int64(), ctypes.c_int64()
+    _check(load().ss_tier_plan(t, b, ctypes.byref(lo), ctypes.byref(hi)), "ss_tier_plan")
+    return lo.value, hi.value
+
+
+def ss_tier_complete(t: int, b: int) -> None:
+    _check(load().ss_tier_complete(t, b), "ss_tier_complete")
+
+
+def ss_download_range(dst_pinned_host: int, src_device: int, nbytes: int, copy_stream: int = 0,
+                      wait_before: Optional[int] = None, signal_after: Optional[int] = None) -> None:
+    _check(load().ss_download_range(dst_pinned_host, src_device, nbytes, copy_stream, wait_before, signal_after),
+           "ss_download_range")

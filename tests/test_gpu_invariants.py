@@ -272,3 +272,74 @@ def test_config5_streamed_layers(stream):
     del host
     for l, b in zip(layers, bufs):
         check_sampled(w, b.out, b.lse, [(3, 2), (30, 7)], layer=l, what=f"config5 streamed layer {l}")
+
+
+def test_tiered_history_round_trip(stream):
+    """Commit-aware tiering (Sec. 4.1): each request's committed history
+    starts on the GPU; the migration Eq. 9 plans moves [0, E) to pinned host
+    memory with ss_download_range, H advances once the copy completed, and a
+    round that attends the Sealed History streamed back from the host plus
+    the GPU-resident Active Tail matches the oracle."""
+    w = W.custom([3000, 1700], [5, 3], num_q_heads=16, num_kv_heads=4, chunk_tokens=4096, seed_base=17)
+    tb = w.num_kv_heads * w.head_dim * 2                       # bytes per token of K (or V)
+    T, g = 512, 256
+    tier = ss.ss_tier_create(w.B, T, g)
+    copy = torch.cuda.Stream()
+    done = ss.ss_event_create()
+    try:
+        dev, host, sealed = [], [], []
+        for b in range(w.B):
+            C = w.hist_len[b]
+            k = w.k_hist(b, device="cuda").contiguous()          # GPU KV cache of request b, token-major
+            v = w.v_hist(b, device="cuda").contiguous()
+            dev.append((k, v))
+            ss.ss_tier_extend(tier, b, C)
+            ss.ss_tier_commit(tier, b, C)
+            lo, hi = ss.ss_tier_plan(tier, b)
+            assert (lo, hi) == (0, ss.ss_tier_endpoint(0, C, T, g)) and hi > 0
+            hk = torch.empty(hi * tb, dtype=torch.uint8).pin_memory()
+            hv = torch.empty(hi * tb, dtype=torch.uint8).pin_memory()
+            torch.cuda.synchronize()
+            ss.ss_download_range(hk.data_ptr(), k.data_ptr(), hi * tb, copy.cuda_stream)
+            ss.ss_download_range(hv.data_ptr(), v.data_ptr(), hi * tb, copy.cuda_stream, None, done)
+            copy.synchronize()
+            ss.ss_tier_complete(tier, b)
+            assert ss.ss_tier_get(tier, b)[0] == hi
+            assert torch.equal(hk, k.view(-1).view(torch.uint8)[: hi * tb].cpu())
+            host.append((hk, hv))
+            sealed.append(hi)
+        print(f"sealed {sealed} of {w.hist_len} tokens", flush=True)
+        # the round: sealed history uploaded into one staging chunk, then each request's tail
+        b_ = H.RoundBuffers(w, max_chunk_tokens=sum(w.hist_len))
+        nb = sum(sealed) * tb
+        stage_k = torch.empty(nb, dtype=torch.uint8, device="cuda")
+        stage_v = torch.empty(nb, dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+        off = 0
+        for b in range(w.B):
+            n = sealed[b] * tb
+            ss.ss_upload_chunk(stage_k.data_ptr() + off, host[b][0].data_ptr(), n, copy.cuda_stream)
+            ss.ss_upload_chunk(stage_v.data_ptr() + off, host[b][1].data_ptr(), n, copy.cuda_stream, None,
+                               done if b == w.B - 1 else None)
+            off += n
+        r = ss.ss_round_init(b_.desc, b_.q.data_ptr(), b_.ws.data_ptr(), b_.ws_bytes, stream.cuda_stream)
+        try:
+            ss.ss_attend_history_chunk(r, stage_k.data_ptr(), stage_v.data_ptr(), sealed, done, None,
+                                       stream.cuda_stream)
+            for b in range(w.B):
+                lens = [0] * w.B
+                lens[b] = w.hist_len[b] - sealed[b]
+                k, v = dev[b]
+                ss.ss_attend_history_chunk(r, k.data_ptr() + sealed[b] * tb, v.data_ptr() + sealed[b] * tb, lens,
+                                           None, None, stream.cuda_stream)
+            ss.ss_attend_local_candidates(r, b_.kc.data_ptr(), b_.vc.data_ptr(), stream.cuda_stream)
+            ss.ss_round_finalize(r, b_.out.data_ptr(), b_.lse.data_ptr(), stream.cuda_stream)
+        finally:
+            ss.ss_round_destroy(r)
+        torch.cuda.synchronize()
+        ref_o, ref_l = oracle_full(w)
+        assert_parity(b_.out.double().cpu().numpy(), ref_o, "tiered round")
+        assert_parity(b_.lse.double().cpu().numpy(), ref_l, "tiered round lse", max_abs=1e-3, rel_l2=1e-4)
+    finally:
+        ss.ss_event_destroy(done)
+        ss.ss_tier_destroy(tier)

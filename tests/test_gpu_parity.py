@@ -143,6 +143,8 @@ def test_small_edge_cases(stream):
         ([4096, 0, 77], [2, 5, 1], 32, 8),
         ([300], [3], 8, 8),              # G = 1
         ([257, 513], [4, 2], 64, 8),     # G = 8: 32 rows per KV head
+        ([700, 64, 1], [4, 1, 2], 8, 1), # Hkv = 1 (multi-query): 8..32 rows per KV head
+        ([5], [8], 4, 1),                # history shorter than the candidate group
     ]
     for k, (lens, cands, hq, hkv) in enumerate(cases):
         w = W.custom(lens, cands, num_q_heads=hq, num_kv_heads=hkv, chunk_tokens=256, seed_base=40 + k)
@@ -163,3 +165,26 @@ def test_valu_and_mfma_paths_agree_with_oracle(stream):
         _full_check(w, b, f"decode mfma_min_rows={mmr}")
         outs.append(b.out.clone())
     assert (outs[0] - outs[1]).abs().max().item() <= 1e-4
+
+
+def test_long_single_request(stream):
+    """One request with 262144 history tokens in one chunk (pieces of the
+    maximum automatic size, chains within one range) and in 3 uneven chunks
+    batched (chains across chunk boundaries)."""
+    for chunk_tokens in (262144, 100000):
+        w = W.custom([262144], [6], num_q_heads=32, num_kv_heads=8, chunk_tokens=chunk_tokens, seed_base=61)
+        print(f"one request x 262144 tokens, chunks of {chunk_tokens}, one batched call", flush=True)
+        b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR, batch=w.num_chunks)
+        check_sampled(w, b.out, b.lse, [(0, 3)], what=f"long request chunks={chunk_tokens}")
+
+
+def test_repeat_is_bitwise_deterministic(stream):
+    """The same sequence of calls gives bitwise the same result (no atomics,
+    fixed slot merge order)."""
+    w = W.workload(4)
+    outs = []
+    for rep in range(2):
+        print(f"config 4 batched, repetition {rep}", flush=True)
+        b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR, batch=w.num_chunks)
+        outs.append((b.out.clone(), b.lse.clone()))
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
