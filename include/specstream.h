@@ -253,6 +253,39 @@ ss_status ss_tier_complete(ss_tier *t, int32_t b);
 ss_status ss_download_range(void *dst_pinned_host, const void *src_device, size_t bytes,
                             hipStream_t copy_stream, hipEvent_t wait_before, hipEvent_t signal_after);
 
+/* ---- I/O-aware dynamic verification width (paper Sec. 4.2) ----------------
+ * Chooses the next round's width q (candidate rows per request, 1..8) as
+ * q* = argmin_q T_round(q) / U(q): estimated round time per committed token.
+ * T_round = max(history transfer, verification compute) + draft generation +
+ * rejection correction (transfer and compute overlap in the pipeline, so
+ * they are not counted twice); U = committed tokens.  Each width is sampled
+ * min_samples times first (ascending); later, widths without records are
+ * estimated from the measured ones (transfer constant in q, compute and
+ * draft time linear in q, U from the geometric acceptance model
+ * (1 - a^q) / (1 - a) fitted to the measured widths).  The width changes
+ * only if the estimate improves on the current one by more than
+ * switch_threshold (a fraction).  Observations are exponentially weighted
+ * with factor `decay` (1 = keep only the latest). */
+typedef struct ss_width_ctl ss_width_ctl;
+
+/* widths: host [num_widths], ascending, each in 1..8; copied. */
+ss_status ss_width_create(ss_width_ctl **out, const int32_t *widths, int32_t num_widths,
+                          double switch_threshold, int32_t min_samples, double decay);
+void ss_width_destroy(ss_width_ctl *c);
+
+/* Record a finished round run at `width`: seconds of history transfer,
+ * verification compute, draft generation and rejection correction, and the
+ * tokens it committed (averaged over the Cohort's requests). */
+ss_status ss_width_observe(ss_width_ctl *c, int32_t width, double transfer_s, double compute_s,
+                           double draft_s, double correct_s, double committed_tokens);
+
+/* The width for the next round (-1 if c is null). */
+int32_t ss_width_select(ss_width_ctl *c);
+
+/* The controller's estimate of seconds per committed token at `width` (-1
+ * for an unknown width). */
+double ss_width_estimate(const ss_width_ctl *c, int32_t width);
+
 /* Event helpers so callers need no HIP binding of their own.  Events are
  * created with timing disabled. */
 ss_status ss_event_create(hipEvent_t *e);

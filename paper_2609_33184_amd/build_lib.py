@@ -34,7 +34,7 @@ def build(verbose: bool = True) -> str:
     kobj = os.path.join(bdir, "ss_kernels.o")
     _run([HIPCC, *COMMON, *DEVICE_ONLY, "-c", os.path.join(CSRC, "ss_kernels.hip"), "-o", kobj])
     objs.append(kobj)
-    for name in ("ss_host", "ss_tier"):
+    for name in ("ss_host", "ss_tier", "ss_width"):
         hobj = os.path.join(bdir, name + ".o")
         _run([HIPCC, *COMMON, "-x", "c++", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", "-c",
               os.path.join(CSRC, name + ".cpp"), "-o", hobj])

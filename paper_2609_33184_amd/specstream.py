@@ -35,6 +35,7 @@ EXPORTED = (
     "ss_status_string", "ss_last_error",
     "ss_tier_endpoint", "ss_tier_create", "ss_tier_destroy", "ss_tier_get", "ss_tier_extend", "ss_tier_commit",
     "ss_tier_plan", "ss_tier_complete", "ss_download_range",
+    "ss_width_create", "ss_width_destroy", "ss_width_observe", "ss_width_select", "ss_width_estimate",
 )
 
 
@@ -88,6 +89,7 @@ def load() -> ctypes.CDLL:
     P, I32, SZ, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t, ctypes.POINTER(ctypes.c_float)
     PI32 = ctypes.POINTER(ctypes.c_int32)
     I64, PI64 = ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)
+    D = ctypes.c_double
     sig = {
         "ss_round_workspace_bytes": (SZ, [ctypes.POINTER(ss_round_desc)]),
         "ss_round_init": (I32, [ctypes.POINTER(P), ctypes.POINTER(ss_round_desc), P, P, SZ, P]),
@@ -114,6 +116,11 @@ def load() -> ctypes.CDLL:
         "ss_tier_plan": (I32, [P, I32, PI64, PI64]),
         "ss_tier_complete": (I32, [P, I32]),
         "ss_download_range": (I32, [P, P, SZ, P, P, P]),
+        "ss_width_create": (I32, [ctypes.POINTER(P), PI32, I32, D, I32, D]),
+        "ss_width_destroy": (None, [P]),
+        "ss_width_observe": (I32, [P, I32, D, D, D, D, D]),
+        "ss_width_select": (I32, [P]),
+        "ss_width_estimate": (D, [P, I32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -267,3 +274,32 @@ def ss_download_range(dst_pinned_host: int, src_device: int, nbytes: int, copy_s
                       wait_before: Optional[int] = None, signal_after: Optional[int] = None) -> None:
     _check(load().ss_download_range(dst_pinned_host, src_device, nbytes, copy_stream, wait_before, signal_after),
            "ss_download_range")
+
+
+# ---------------------------------------------------------------------------
+# dynamic verification width (paper Sec. 4.2)
+# ---------------------------------------------------------------------------
+def ss_width_create(widths: Sequence[int], switch_threshold: float = 0.05, min_samples: int = 2,
+                    decay: float = 0.25) -> int:
+    h = ctypes.c_void_p()
+    _check(load().ss_width_create(ctypes.byref(h), _lens(widths), len(widths), switch_threshold, min_samples,
+                                  decay), "ss_width_create")
+    return h.value
+
+
+def ss_width_destroy(c: Optional[int]) -> None:
+    load().ss_width_destroy(c)
+
+
+def ss_width_observe(c: int, width: int, transfer_s: float, compute_s: float, draft_s: float, correct_s: float,
+                     committed_tokens: float) -> None:
+    _check(load().ss_width_observe(c, width, transfer_s, compute_s, draft_s, correct_s, committed_tokens),
+           "ss_width_observe")
+
+
+def ss_width_select(c: int) -> int:
+    return int(load().ss_width_select(c))
+
+
+def ss_width_estimate(c: int, width: int) -> float:
+    return float(load().ss_width_estimate(c, width))
