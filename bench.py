@@ -136,9 +136,24 @@ def cpu_baseline(w, chunks, sample_requests):
     dt = time.perf_counter() - t0
     nbytes = sum((w.hist_len[b] + w.num_cand[b]) * w.token_bytes() for b in sample_requests)
     cores = len(os.sched_getaffinity(0))
+    # the same oracle limited to one BLAS thread, on the first sampled request
+    one = None
+    try:
+        from threadpoolctl import threadpool_limits
+        q, kh, vh, kc, vc = host[0]
+        with threadpool_limits(limits=1):
+            t1 = time.perf_counter()
+            oracle.verify_attention([bf16_bits_to_f64(q)], [bf16_bits_to_f64(kh)], [bf16_bits_to_f64(vh)],
+                                    [bf16_bits_to_f64(kc)], [bf16_bits_to_f64(vc)], scale=w.softmax_scale)
+            d1 = time.perf_counter() - t1
+        b0 = sample_requests[0]
+        one = {"value": round((w.hist_len[b0] + w.num_cand[b0]) * w.token_bytes() / d1 / 1e9, 4), "unit": "GB/s",
+               "cores": 1, "seconds": round(d1, 3), "sample": f"request {b0} only"}
+    except Exception:  # pragma: no cover
+        one = None
     return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": blas_threads or cores,
             "host_cores_available": cores, "kind": "oracle",
-            "seconds": round(dt, 3),
+            "seconds": round(dt, 3), "one_thread": one,
             "sample": f"fp64 numpy oracle (direct masked softmax) over {len(sample_requests)} of {w.B} requests "
                       f"(all 32 query heads, {w.hist_len[0]} history + {w.num_cand[0]} candidate tokens each), "
                       f"same seeded inputs; GB/s of KV processed"}
@@ -384,6 +399,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--split-tokens", type=int, default=0)
+    ap.add_argument("--num-cand", type=int, default=0,
+                    help="override the candidate count of every request (1 = plain decode: "
+                         "4 rows per KV head, which the VALU body attends)")
     ap.add_argument("--batch", type=int, default=0,
                     help="history chunks per ss_attend_history_chunks call in the timed round "
                          "(0 = all resident chunks in one call, 1 = one call per chunk)")
@@ -429,6 +447,9 @@ def main() -> int:
         return 0
     ss.load()
     w = W.workload(args.config)
+    if args.num_cand > 0:
+        w = W.custom(w.hist_len, [args.num_cand] * w.B, num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads,
+                     head_dim=w.head_dim, chunk_tokens=w.chunk_tokens, cfg_id=args.config)
     log(f"bench: config {args.config} ({w.name}): generating inputs on the GPU")
     layout = ss.SS_KV_HEAD_MAJOR if args.kv_layout == "head" else ss.SS_KV_TOKEN_MAJOR
     b = H.RoundBuffers(w, split_tokens=args.split_tokens, kv_layout=layout)

@@ -11,7 +11,7 @@ Sec. 4.2 of the paper, "KV Streaming for Multi-Query Verification":
 * Eq. 13 / Eq. 14: chunk-local (m_j, l_j, a_j) and the rescaled merge,
   state initialised to (-inf, 0, 0) per query and head; O = a / l at the end.
 
-Readings (listed in the design doc as well): query head h reads KV head
+Readings where the paper leaves a choice: query head h reads KV head
 floor(h / G) with G = Hq / Hkv (contiguous GQA groups); Q and K arrive with
 positional encoding already applied; the scale is sigma = 1/sqrt(d).
 

@@ -374,7 +374,7 @@ def _log_uniform_lengths(cfg_id: int, B: int, lo: int, hi: int) -> Tuple[List[in
 
 
 def workload(cfg_id: int) -> Workload:
-    """The five configurations of the build (input recipe)."""
+    """The five workload configurations (seeded synthetic inputs of the paper's shapes)."""
     if cfg_id == 1:
         return Workload(1, "tiny-1req-8q2kv-4096ctx", 8, 2, 128, 1024, [4096], [5])
     if cfg_id == 2:

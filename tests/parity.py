@@ -1,6 +1,6 @@
 """Parity helpers: compare GPU outputs with the fp64 oracle (test helper).
 
-The bar (the benchmark spec): max-abs error <= 2e-3 and relative L2 error <= 1e-3 on
+The bar: max-abs error <= 2e-3 and relative L2 error <= 1e-3 on
 the fp32 outputs, for bf16 inputs with fp32 accumulation.
 """
 from __future__ import annotations
