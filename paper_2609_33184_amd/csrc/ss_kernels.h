@@ -59,7 +59,12 @@ struct State {
   int32_t R;        // rows = sum n_b * Hq
 };
 
-struct ChunkParams {
+// Kernel arguments.  The unit and item tables travel by value in the
+// kernel-argument segment; the launch wrappers pick the smallest of three
+// table capacities that holds a launch, so a typical round passes a few KB
+// (large by-value arguments fill the runtime's argument pool quickly, and a
+// full pool makes the next launch wait for the queue to drain).
+struct ChunkHeader {
   const uint16_t *q;    // bf16 [sum n_b, Hq, d]
   State st;
   int32_t Hq, Hkv, G;
@@ -71,13 +76,20 @@ struct ChunkParams {
   const uint16_t *v[kMaxChunks];
   uint64_t head_stride[kMaxChunks];   // elements between KV heads at the same token
   int32_t num_units;
-  // unit u = items [units[u] & 0xffff, + ((units[u] >> 16) & 0xff)), 1..kMaxChain
-  // items, attended by the body units[u] >> 24 (kUnitValu / kUnitMfma1 / kUnitMfma2)
-  uint32_t units[kMaxUnits];
-  Item items[kMaxItems];
 };
 
-struct FinalParams {
+template <int MaxUnits, int MaxItems>
+struct ChunkParamsT : ChunkHeader {
+  static constexpr int kUnits = MaxUnits;
+  static constexpr int kItems = MaxItems;
+  // unit u = items [units[u] & 0xffff, + ((units[u] >> 16) & 0xff)), 1..kMaxChain
+  // items, attended by the body units[u] >> 24 (kUnitValu / kUnitMfma1 / kUnitMfma2)
+  uint32_t units[MaxUnits];
+  Item items[MaxItems];
+};
+using ChunkParams = ChunkParamsT<kMaxUnits, kMaxItems>;   // what the host fills
+
+struct FinalHeader {
   const uint16_t *kc;   // bf16 candidate K [sum n_b, Hkv, d]
   const uint16_t *vc;   // bf16 candidate V
   const uint16_t *q;
@@ -87,8 +99,14 @@ struct FinalParams {
   int32_t Hq, Hkv, G;
   float scale_log2;
   int32_t num_items;
-  Item items[kMaxItems];
 };
+
+template <int MaxItems>
+struct FinalParamsT : FinalHeader {
+  static constexpr int kItems = MaxItems;
+  Item items[MaxItems];
+};
+using FinalParams = FinalParamsT<kMaxItems>;
 
 // Launch wrappers; return hipGetLastError() of the launch.
 // History units of every kind, grid (num_units, Hkv).

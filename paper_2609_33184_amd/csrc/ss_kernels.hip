@@ -21,6 +21,8 @@
 
 #include "ss_kernels.h"
 
+#include <cstring>
+
 #include <math.h>
 
 #include <type_traits>
@@ -35,6 +37,11 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr int kAwPitch = 132;  // floats per row of a wave's partial accumulator
 constexpr int kBufferFlags = 0x00020000;   // buffer resource word 3: 32-bit data format, raw offsets
+// Cache policy of the history K/V loads: non-temporal.  Every history byte
+// is read once per round, so the streaming loads should not displace
+// reusable lines; measured on MI355X, this took config 3's round from 378 to
+// 354 us and config 4's from 786 to 743 us (means over 40 rounds).
+constexpr int kStreamLoad = 2;
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -67,7 +74,8 @@ __device__ __forceinline__ float xgroup_sum(float x) {
   return x;
 }
 
-__device__ __forceinline__ int global_row(const ChunkParams &p, const Item &it, int g, int r) {
+template <typename P>
+__device__ __forceinline__ int global_row(const P &p, const Item &it, int g, int r) {
   // local row r of (request, kv head g) -> packed query row (off_b + i) * Hq + h
   const int i = r / p.G;
   const int h = g * p.G + (r - i * p.G);
@@ -80,8 +88,8 @@ __device__ __forceinline__ int global_row(const ChunkParams &p, const Item &it, 
 // all relative to their own maxima); combine them (Eq. 14 over the waves) and
 // fold the result into the item's slot of the running state (Eq. 14 again).
 // ---------------------------------------------------------------------------
-template <int ROWS>
-__device__ __forceinline__ void fold_into_slot(const ChunkParams &p, const Item &it, int g, int M,
+template <int ROWS, typename P>
+__device__ __forceinline__ void fold_into_slot(const P &p, const Item &it, int g, int M,
                                                const float *aw, const float *mw, const float *lw) {
   // SEGS threads per row, SEGLEN (a multiple of 4) values each
   constexpr int SEGS = (256 / ROWS) < 32 ? (256 / ROWS) : 32;
@@ -196,7 +204,8 @@ __device__ __forceinline__ int tiles_of(const Item &it) { return (it.tok_count +
 // (p.k or p.v): loads past the item's last token return zero, so no
 // clamping is needed.  Offsets are 32-bit (the host keeps an item below
 // 2^31 bytes).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t item_rsrc(const ChunkParams &p, const Item &it, int g,
+template <typename P>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t item_rsrc(const P &p, const Item &it, int g,
                                                             const uint16_t *const *tab) {
   const uint32_t nrec = (uint32_t)(it.tok_count - 1) * (p.tok_stride * 2) + kRowBytes;
   const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride[it.chunk];
@@ -211,7 +220,8 @@ struct TileCursor {
   int k = 0;
   int base = 0;
 };
-__device__ __forceinline__ void seek(const ChunkParams &p, int i0, int nit, TileCursor &c, int T) {
+template <typename P>
+__device__ __forceinline__ void seek(const P &p, int i0, int nit, TileCursor &c, int T) {
   while (c.k + 1 < nit && T - c.base >= tiles_of(p.items[i0 + c.k])) {
     c.base += tiles_of(p.items[i0 + c.k]);
     ++c.k;
@@ -239,8 +249,8 @@ __device__ __forceinline__ s16x4_t lds_read_tr16(const unsigned char *p) {
       (__attribute__((address_space(3))) s16x4_t *)(reinterpret_cast<uintptr_t>(p)));
 }
 
-template <int RB>
-__device__ __forceinline__ void mfma_unit(const ChunkParams &p, unsigned char *smem, int i0, int nit) {
+template <int RB, typename P>
+__device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i0, int nit) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15;
@@ -276,10 +286,10 @@ __device__ __forceinline__ void mfma_unit(const ChunkParams &p, unsigned char *s
   auto load_kv = [&](const NextTile &nx) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.krs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, 0);
+      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.krs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, kStreamLoad);
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.vrs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, 0);
+      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.vrs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, kStreamLoad);
   };
   // K operand read: row 16u + lr, chunk 4s + lq at position (4s + lq) ^ lr
   // V transpose read: row 4lq + lr/4 (+16), chunk 2db + (lr&3)/2, half lr&1
@@ -468,8 +478,8 @@ __device__ __forceinline__ void mfma_unit(const ChunkParams &p, unsigned char *s
 // coalesced loads (4 token rows of 256 B each) of K and of V.  Scores are
 // reduced over the 16 lanes of a DPP row.
 // ---------------------------------------------------------------------------
-template <int MAXR>
-__device__ __forceinline__ void valu_unit(const ChunkParams &p, float *smem, int i0, int nit) {
+template <int MAXR, typename P>
+__device__ __forceinline__ void valu_unit(const P &p, float *smem, int i0, int nit) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int lane = threadIdx.x & 63;
   const int c = lane & 15;
@@ -513,12 +523,12 @@ __device__ __forceinline__ void valu_unit(const ChunkParams &p, float *smem, int
   auto load_k = [&](const NextTile &nx) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.krs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, 0);
+      kr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.krs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, kStreamLoad);
   };
   auto load_v = [&](const NextTile &nx) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.vrs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, 0);
+      vr[i] = __builtin_amdgcn_raw_buffer_load_b128(nx.vrs, voff + (uint32_t)(nx.tb + 4 * i) * stride_b, 0, kStreamLoad);
   };
   // one tile per iteration (tokens [tb, tb + 32) of an item with `count`
   // tokens); the next tile's K is issued after the scores, its V after the
@@ -648,7 +658,8 @@ static_assert(MfmaLds<1>::kBytes <= kChunkLdsBytes, "LDS sizes");
 // launch keeps the whole call in a single wave of workgroups whatever the
 // mix of candidate counts in the Cohort.
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256, 2) chunk_attn(const ChunkParams p) {
+template <typename P>
+__global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[kChunkLdsBytes];
   const uint32_t unit = p.units[blockIdx.x];
   const int i0 = unit & 0xffff;
@@ -679,7 +690,8 @@ __global__ void __launch_bounds__(256, 2) chunk_attn(const ChunkParams p) {
 // ---------------------------------------------------------------------------
 constexpr int kFinGroup = 16;
 
-__global__ void __launch_bounds__(256) finalize_kernel(const FinalParams p) {
+template <typename P>
+__global__ void __launch_bounds__(256) finalize_kernel(const P p) {
   const int w = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const Item it = p.items[blockIdx.x];
@@ -772,15 +784,48 @@ __global__ void __launch_bounds__(256) finalize_kernel(const FinalParams p) {
 
 }  // namespace
 
+namespace {
+
+// Table capacities of the launches: a Cohort's whole history call usually
+// fits the small class (config 3: 32 units, 128 items), large ragged
+// batches the medium one.
+using ChunkSmall = ChunkParamsT<64, 256>;
+using ChunkMedium = ChunkParamsT<256, 1024>;
+using FinalSmall = FinalParamsT<64>;
+
+template <typename D>
+hipError_t launch_chunk_as(const ChunkParams &p, hipStream_t s) {
+  static thread_local D d;
+  static_cast<ChunkHeader &>(d) = p;
+  std::memcpy(d.units, p.units, sizeof(uint32_t) * p.num_units);
+  std::memcpy(d.items, p.items, sizeof(Item) * p.num_items);
+  hipLaunchKernelGGL(chunk_attn<D>, dim3(p.num_units, p.Hkv), dim3(256), 0, s, d);
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_chunk(const ChunkParams &p, hipStream_t s) {
-  hipLaunchKernelGGL(chunk_attn, dim3(p.num_units, p.Hkv), dim3(256), 0, s, p);
+  if (p.num_units <= ChunkSmall::kUnits && p.num_items <= ChunkSmall::kItems)
+    return launch_chunk_as<ChunkSmall>(p, s);
+  if (p.num_units <= ChunkMedium::kUnits && p.num_items <= ChunkMedium::kItems)
+    return launch_chunk_as<ChunkMedium>(p, s);
+  hipLaunchKernelGGL(chunk_attn<ChunkParams>, dim3(p.num_units, p.Hkv), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
 hipError_t launch_finalize(const FinalParams &p, hipStream_t s) {
   int rows = 0;
   for (int i = 0; i < p.num_items; ++i) rows = rows > p.items[i].n_cand * p.Hq ? rows : p.items[i].n_cand * p.Hq;
-  hipLaunchKernelGGL(finalize_kernel, dim3(p.num_items, (rows + kWaves - 1) / kWaves), dim3(256), 0, s, p);
+  const dim3 grid(p.num_items, (rows + kWaves - 1) / kWaves);
+  if (p.num_items <= FinalSmall::kItems) {
+    static thread_local FinalSmall d;
+    static_cast<FinalHeader &>(d) = p;
+    std::memcpy(d.items, p.items, sizeof(Item) * p.num_items);
+    hipLaunchKernelGGL(finalize_kernel<FinalSmall>, grid, dim3(256), 0, s, d);
+  } else {
+    hipLaunchKernelGGL(finalize_kernel<FinalParams>, grid, dim3(256), 0, s, p);
+  }
   return hipGetLastError();
 }
 
