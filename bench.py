@@ -236,7 +236,7 @@ def config_table(torch, H, ss, W, stream, layout: int, rounds: int):
         flush = torch.zeros(1 << 27, dtype=torch.int32, device="cuda") if w.history_kv_bytes() < (1 << 28) else None
         torch.cuda.synchronize()
         batch = w.num_chunks
-        round_times(torch, H, b, chunks, stream, 2, batch, flush)
+        round_times(torch, H, b, chunks, stream, 20, batch, flush)   # clocks settle (see --warmup)
         t = round_times(torch, H, b, chunks, stream, rounds, batch, flush)
         kv = w.algorithmic_kv_bytes()
         p50 = pct(t, 0.5)

@@ -49,14 +49,18 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // (query staging, wave merge, state fold) and a single wave of workgroups
 // has no hand-over between them; aim for one workgroup per CU (256 on
 // MI355X) per launch.  A piece may span chunks of a batched call.  Measured
-// on 16 x 32768 tokens, 8 KV heads: 1024 workgroups of 4096 tokens 394 us,
-// 512 of 8192 384 us, 256 of 16384 381 us per round.  On 64 requests of
-// 2048..65536 tokens, pieces of about an eighth of the per-CU share balance
-// best (4096 tokens: 801 us, 8192: 826 us, 16384: 864 us, 36864: 915 us).
+// per round with non-temporal K/V loads: 16 x 32768 tokens, 8 KV heads:
+// pieces of 8192 tokens 340 us, 16384 (the rule) 329 us, 32768 462 us;
+// 32 x 131072 tokens: 16384 2636 us, 32768 2577 us, 65536 and 131072 (the
+// rule) 2545 us.  Ragged requests make pieces of unequal size, which the
+// longest-first order balances only with several pieces per CU; on 64
+// requests of 2048..65536 tokens a sixth of the per-CU share measured best
+// (pieces of 4096 tokens: 718 us, 8448: 714, 11264: 673, 12288: 668,
+// 14336: 723, 16384: 678).
 constexpr long kTargetWorkgroups = 256;
-constexpr long kRaggedSplit = 8;   // units per CU when request lengths differ
+constexpr long kRaggedSplit = 6;   // pieces per CU share when request lengths differ
 constexpr int kMinPiece = 256;
-constexpr int kMaxAutoPiece = 32768;
+constexpr int kMaxAutoPiece = 131072;
 constexpr int kDefaultMfmaMinRows = ss::kMaxValuRows + 1;
 
 ss_status validate_desc(const ss_round_desc *d) {

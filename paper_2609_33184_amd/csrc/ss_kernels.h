@@ -109,7 +109,7 @@ struct FinalParamsT : FinalHeader {
 using FinalParams = FinalParamsT<kMaxItems>;
 
 // Launch wrappers; return hipGetLastError() of the launch.
-// History units of every kind, grid (num_units, Hkv).
+// History units of every kind, grid (Hkv, num_units).
 hipError_t launch_chunk(const ChunkParams &p, hipStream_t s);
 // Speculative Frontier pass fused with the split-slot merge and O = a / l.
 hipError_t launch_finalize(const FinalParams &p, hipStream_t s);
