@@ -403,8 +403,10 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--split-tokens", type=int, default=0)
     ap.add_argument("--num-cand", type=int, default=0,
-                    help="override the candidate count of every request (1 = plain decode: "
-                         "4 rows per KV head, which the VALU body attends)")
+                    help="override the candidate count of every request (1 = plain decode: 4 rows per KV head)")
+    ap.add_argument("--mfma-min-rows", type=int, default=0,
+                    help="ss_round_desc.mfma_min_rows (0 = the library's default, always MFMA; "
+                         "5 = the fp32 VALU body for up to 4 rows per KV head)")
     ap.add_argument("--batch", type=int, default=0,
                     help="history chunks per ss_attend_history_chunks call in the timed round "
                          "(0 = all resident chunks in one call, 1 = one call per chunk)")
@@ -455,7 +457,7 @@ def main() -> int:
                      head_dim=w.head_dim, chunk_tokens=w.chunk_tokens, cfg_id=args.config)
     log(f"bench: config {args.config} ({w.name}): generating inputs on the GPU")
     layout = ss.SS_KV_HEAD_MAJOR if args.kv_layout == "head" else ss.SS_KV_TOKEN_MAJOR
-    b = H.RoundBuffers(w, split_tokens=args.split_tokens, kv_layout=layout)
+    b = H.RoundBuffers(w, split_tokens=args.split_tokens, kv_layout=layout, mfma_min_rows=args.mfma_min_rows)
     chunks = H.hbm_history(w, kv_layout=layout)
     stream = torch.cuda.Stream()
     torch.cuda.synchronize()

@@ -83,8 +83,9 @@ typedef struct {
                                else a multiple of 32                           */
   int32_t mfma_min_rows;    /* rows per KV head (n_b * G) from which the bf16
                                MFMA path is used; fewer (at most 4) use the
-                               fp32 VALU path.  0 = default (5: groups of <= 4
-                               rows on VALU); 1 = always MFMA; range 0..5      */
+                               fp32 VALU path.  0 = default (1: always MFMA,
+                               the faster body at every row count); 2..5 =
+                               VALU below that many rows; range 0..5           */
   int32_t kv_layout;        /* layout of history chunks: SS_KV_TOKEN_MAJOR
                                [sum_b len_b][Hkv][d] or SS_KV_HEAD_MAJOR
                                [Hkv][sum_b len_b][d]                           */

@@ -61,7 +61,11 @@ constexpr long kTargetWorkgroups = 256;
 constexpr long kRaggedSplit = 6;   // pieces per CU share when request lengths differ
 constexpr int kMinPiece = 256;
 constexpr int kMaxAutoPiece = 131072;
-constexpr int kDefaultMfmaMinRows = ss::kMaxValuRows + 1;
+// Body for few rows per KV head: the MFMA body with padded rows by default.
+// With non-temporal K/V loads the fp32 VALU body became compute-bound (VALU
+// 72% busy): 16 x 32768 tokens with 4 rows per KV head took 396-399 us on
+// VALU and 330-345 us on MFMA; 64 ragged requests 710 and 695 us.
+constexpr int kDefaultMfmaMinRows = 1;
 
 ss_status validate_desc(const ss_round_desc *d) {
   if (d == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "desc is null");

@@ -68,7 +68,7 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
       for (int bb = 0; bb < B; ++bb) if (off_rows[bb] == it.q_row0) b = bb;
       CHECK(b >= 0, "q_row0");
       const int M = it.n_cand * G;
-      const int want_kind = (M < (mfma_min_rows ? mfma_min_rows : 5) && M <= 4) ? 0 : (M <= 16 ? 1 : 2);
+      const int want_kind = (M < (mfma_min_rows ? mfma_min_rows : 1) && M <= 4) ? 0 : (M <= 16 ? 1 : 2);
       CHECK(kind == want_kind, "unit kind %d want %d (M=%d)", kind, want_kind, M);
       int ntiles = 0;
       long toks = 0;

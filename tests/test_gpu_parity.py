@@ -148,7 +148,7 @@ def test_small_edge_cases(stream):
     ]
     for k, (lens, cands, hq, hkv) in enumerate(cases):
         w = W.custom(lens, cands, num_q_heads=hq, num_kv_heads=hkv, chunk_tokens=256, seed_base=40 + k)
-        for mfma_min_rows in (0, 1):
+        for mfma_min_rows in (5, 1):     # 5: groups of <= 4 rows on the VALU body; 1: all MFMA
             for layout in LAYOUTS:
                 print(f"edge case {k}: lens={lens} cands={cands} Hq={hq} Hkv={hkv} "
                       f"mfma_min_rows={mfma_min_rows} layout={layout}", flush=True)
