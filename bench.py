@@ -41,9 +41,18 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_33184_amd", "csrc", "ss_kernels.hip"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "chunk_attn_config3_traffic.json")
 
 
+def code_hash(text: str) -> str:
+    """sha256[:16] of C++ source with its comments and whitespace removed, so
+    a comment edit does not invalidate counters taken on the same code."""
+    import re
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return hashlib.sha256("".join(text.split()).encode()).hexdigest()[:16]
+
+
 def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    with open(KERNEL_SRC) as f:
+        return code_hash(f.read())
 
 
 def log(msg: str) -> None:
@@ -501,7 +510,7 @@ def main() -> int:
     if os.path.exists(TRAFFIC_FILE):
         try:
             tr = json.load(open(TRAFFIC_FILE))
-            if tr.get("kernel_source_sha256_16") == kernel_source_hash() and tr.get("config") == args.config:
+            if tr.get("kernel_code_sha256_16") == kernel_source_hash() and tr.get("config") == args.config:
                 traffic = tr.get("hbm_bytes_per_launch")
         except Exception:
             traffic = None

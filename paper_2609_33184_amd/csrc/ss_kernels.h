@@ -30,7 +30,7 @@ constexpr int kSlotFresh = 1;
 
 // History item: one token range of one chunk for one request: tokens
 // [tok_begin, tok_begin + tok_count) of chunk `chunk` (tok_count >= 1).
-// A unit (one workgroup per KV head, blockIdx.y) is a chain of consecutive
+// A unit (one workgroup per KV head, blockIdx.x) is a chain of consecutive
 // items of one request, attended as one token sequence with one running
 // state that is folded into split slot `slot`; every item of a chain carries
 // the same q_row0, n_cand, slot and flags.

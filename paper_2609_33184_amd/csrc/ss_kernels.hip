@@ -159,7 +159,7 @@ __device__ __forceinline__ void fold_into_slot(const P &p, const Item &it, int g
 }
 
 // ---------------------------------------------------------------------------
-// MFMA chunk body.  Workgroup = (unit, kv head); 4 waves; wave w takes the
+// MFMA chunk body.  Workgroup = (kv head, unit); 4 waves; wave w takes the
 // 32-token tiles w, w+4, ... of the unit's chain of items (one request's
 // token ranges, possibly from several chunks, attended as one sequence).
 // Per tile:
@@ -472,8 +472,9 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i
 }
 
 // ---------------------------------------------------------------------------
-// VALU chunk body for sparse query groups (few rows per KV head): fp32 dot
-// products on the vector ALUs, exact fp32 softmax weights.  Lane l: d-chunk
+// VALU chunk body for sparse query groups (few rows per KV head), used when
+// the round's mfma_min_rows asks for it: fp32 dot products on the vector
+// ALUs, exact fp32 softmax weights.  Lane l: d-chunk
 // c = l % 16 (8 values), token group tg = l / 16; a 32-token tile is 8
 // coalesced loads (4 token rows of 256 B each) of K and of V.  Scores are
 // reduced over the 16 lanes of a DPP row.
@@ -655,9 +656,9 @@ static_assert(MfmaLds<1>::kBytes <= kChunkLdsBytes, "LDS sizes");
 // History kernel: one launch for every unit of a call.  Workgroup =
 // (kv head, unit) = (blockIdx.x, blockIdx.y); the unit's kind (from the
 // unit table) selects the body: MFMA with two or one 16-row blocks, or the
-// VALU path for <= 4 rows.  One launch keeps the whole call in a single wave
-// of workgroups whatever the mix of candidate counts in the Cohort.  The
-// heads are the fast grid dimension, so workgroups start in the unit
+// VALU path for <= 4 rows (when the round asks for it).  One launch keeps
+// the whole call in a single wave of workgroups whatever the mix of
+// candidate counts in the Cohort.  The heads are the fast grid dimension, so workgroups start in the unit
 // table's longest-first order across all heads, and with 8 KV heads the
 // round-robin placement gives every XCD one head of every unit (measured on
 // 64 ragged requests: 749-754 us with the unit-major grid, 731 us).
