@@ -45,22 +45,19 @@ using ss::hip_fail;
 inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Automatic piece size: large pieces amortise each workgroup's fixed costs
-// (query staging, wave merge, state fold) and a single wave of workgroups
-// has no hand-over between them; aim for one workgroup per CU (256 on
-// MI355X) per launch.  A piece may span chunks of a batched call.  Measured
-// per round with non-temporal K/V loads: 16 x 32768 tokens, 8 KV heads:
-// pieces of 8192 tokens 340 us, 16384 (the rule) 329 us, 32768 462 us;
-// 32 x 131072 tokens: 16384 2636 us, 32768 2577 us, 65536 and 131072 (the
-// rule) 2545 us.  Ragged requests make pieces of unequal size, which the
-// longest-first order balances only with several pieces per CU; on 64
-// requests of 2048..65536 tokens a sixth of the per-CU share measured best
-// (pieces of 4096 tokens: 718 us, 8448: 714, 11264: 673, 12288: 668,
-// 14336: 723, 16384: 678).
+// Workgroups of a history call: the call's tokens (every request's, in
+// request order) are cut into equal shares, one per workgroup and KV head
+// (stream-K style), so every workgroup has the same work however ragged the
+// requests are; a share may span several requests.  Large shares amortise
+// each unit's fixed costs (query staging, wave merge, state fold); aim for
+// one workgroup per CU (256 on MI355X).  Measured per round: 16 x 32768
+// tokens, 8 KV heads: shares of 8192 tokens (512 workgroups) 340 us, 16384
+// (256) 329 us; 32 x 131072 tokens: 256 workgroups 2545 us, 1024 2577 us.
+// 64 ragged requests of 2048..65536 tokens took 698-702 us with
+// per-request pieces in longest-first order and 678-681 us with equal
+// shares (same GPU, same run).
 constexpr long kTargetWorkgroups = 256;
-constexpr long kRaggedSplit = 6;   // pieces per CU share when request lengths differ
-constexpr int kMinPiece = 256;
-constexpr int kMaxAutoPiece = 131072;
+constexpr int kMinPiece = 256;   // tokens per workgroup at least
 // Body for few rows per KV head: the MFMA body with padded rows by default.
 // With non-temporal K/V loads the fp32 VALU body became compute-bound (VALU
 // 72% busy): 16 x 32768 tokens with 4 rows per KV head took 396-399 us on
@@ -178,137 +175,149 @@ ss_status check_history_args(const ss_round *r, int nchunks, const void *const *
   return SS_OK;
 }
 
-// Work of one history call: chains of items, chain c = items[start[c] ..
-// start[c + 1]) (one request, one state slot), attended by kernel body kind[c].
-struct Chains {
-  std::vector<ss::Item> items;
-  std::vector<uint32_t> start{0};
-  std::vector<uint8_t> kind;
-  size_t size() const { return start.size() - 1; }
-  long tokens(size_t c) const {
-    long n = 0;
-    for (uint32_t i = start[c]; i < start[c + 1]; ++i) n += items[i].tok_count;
-    return n;
-  }
-};
-
+// Work of one history call.  Unit u = items [unit_first[u],
+// unit_first[u + 1]): a chain of at most kMaxChain token ranges of one
+// request, attended as one sequence into its own state slot by body
+// kind[u].  Workgroup w (of every KV head) attends units [wg_first[w],
+// wg_first[w + 1]) in order.
 struct Plan {
-  Chains chains;
+  std::vector<ss::Item> items;
+  std::vector<uint32_t> unit_first{0};
+  std::vector<uint8_t> kind;
+  std::vector<uint32_t> wg_first;
   std::vector<int32_t> slots_after;   // per request: slots in use after this call
+  size_t units() const { return kind.size(); }
 };
 
-// Kernel body of request b's units: VALU for few rows per KV head, else MFMA
-// with one or two 16-row blocks.
+// Kernel body of request b's units: VALU for few rows per KV head when the
+// round asks for it, else MFMA with one or two 16-row blocks.
 int kind_of(const ss_round *r, int b) {
   const int min_rows = r->mfma_min_rows > 0 ? r->mfma_min_rows : kDefaultMfmaMinRows;
   const int M = r->n_cand[b] * r->G;
   return (M < min_rows && M <= ss::kMaxValuRows) ? ss::kUnitValu : (M <= 16) ? ss::kUnitMfma1 : ss::kUnitMfma2;
 }
 
-// Cut every request's tokens of this call (its ranges in chunk order, as one
-// sequence) into n_b = ceil(L_b / piece) pieces of equal size (a multiple of
-// the tile, the last one shorter); a piece is a chain of at most kMaxChain
-// ranges (a chunk boundary starts a new range) and gets its own state slot.
-// Returns false if a request would need more than kNumSlots slots.
-bool build_plan(const ss_round *r, int nchunks, const int32_t *len, long piece, Plan *plan) {
+// Split this call's tokens into W shares.  The requests' tokens (each
+// request's ranges in chunk order) are concatenated in request order; share
+// w is [x_w, x_{w+1}) with x_w = w * L / W moved down to a tile boundary of
+// its request.  Inside a share, each request's part becomes units: its
+// token ranges, cut at chunk boundaries and at pmax tokens, in chains of at
+// most kMaxChain.  Returns false if a request would need more than
+// kNumSlots slots.
+bool build_plan(const ss_round *r, int nchunks, const int32_t *len, long W, long pmax, Plan *plan) {
+  const int B = r->B;
   *plan = Plan();
   plan->slots_after = r->slots_used;
-  Chains *dst = &plan->chains;
-  std::vector<long> off(nchunks, 0);   // first token of request b in chunk c
-  for (int b = 0; b < r->B; ++b) {
-    const int kind = kind_of(r, b);
-    long L = 0;
-    for (int c = 0; c < nchunks; ++c) L += len[(size_t)c * r->B + b];
-    const long n = (L + piece - 1) / piece;
-    const long pb = n > 0 ? (long)align_up((size_t)((L + n - 1) / n), ss::kTile) : piece;
-    int slot = 0;
-    long filled = 0;      // tokens in the open chain
-    int ranges = 0;       // items in the open chain
-    auto close = [&]() {
-      if (ranges == 0) return;
-      dst->start.push_back((uint32_t)dst->items.size());
-      dst->kind.push_back((uint8_t)kind);
-      ++slot;
-      filled = 0;
-      ranges = 0;
-    };
-    for (int c = 0; c < nchunks; ++c) {
-      const long nc = len[(size_t)c * r->B + b];
-      long p0 = 0;
-      while (p0 < nc) {
-        if (filled == pb || ranges == ss::kMaxChain) close();
-        if (slot >= ss::kNumSlots) return false;
-        const long take = std::min(nc - p0, pb - filled);
-        ss::Item it;
-        it.tok_begin = (int32_t)(off[c] + p0);
-        it.tok_count = (int32_t)take;
-        it.q_row0 = r->row_off[b];
-        it.n_cand = (uint8_t)r->n_cand[b];
-        it.chunk = (uint8_t)c;
-        it.slot = (uint8_t)slot;
-        it.flags = slot >= r->slots_used[b] ? ss::kSlotFresh : 0;
-        dst->items.push_back(it);
-        ++ranges;
-        filled += take;
-        p0 += take;
-      }
-      off[c] += nc;
+  // per request: tokens before chunk c (cum), and offset of the request in chunk c (off)
+  std::vector<long> cum((size_t)B * (nchunks + 1), 0), off((size_t)nchunks * B, 0), start(B + 1, 0);
+  for (int c = 0; c < nchunks; ++c) {
+    long o = 0;
+    for (int b = 0; b < B; ++b) {
+      off[(size_t)c * B + b] = o;
+      o += len[(size_t)c * B + b];
     }
-    close();
-    plan->slots_after[b] = std::max(plan->slots_after[b], slot);
   }
+  for (int b = 0; b < B; ++b) {
+    for (int c = 0; c < nchunks; ++c)
+      cum[(size_t)b * (nchunks + 1) + c + 1] = cum[(size_t)b * (nchunks + 1) + c] + len[(size_t)c * B + b];
+    start[b + 1] = start[b] + cum[(size_t)b * (nchunks + 1) + nchunks];
+  }
+  const long L = start[B];
+  std::vector<long> x(W + 1, L);
+  x[0] = 0;
+  for (long w = 1, b = 0; w < W; ++w) {
+    const long raw = L * w / W;
+    while (start[b + 1] <= raw) ++b;
+    const long o = raw - start[b];
+    x[w] = std::max(x[w - 1], start[b] + o - o % ss::kTile);
+  }
+  std::vector<int> slot(B, 0);
+  long ranges = 0;   // items in the open unit
+  int ub = -1;       // request of the open unit
+  auto close = [&]() {
+    if (ranges == 0) return true;
+    plan->unit_first.push_back((uint32_t)plan->items.size());
+    plan->kind.push_back((uint8_t)kind_of(r, ub));
+    ++slot[ub];
+    ranges = 0;
+    return true;
+  };
+  for (long w = 0; w < W; ++w) {
+    plan->wg_first.push_back((uint32_t)plan->units());
+    long pos = x[w];
+    int b = 0;
+    while (b < B && start[b + 1] <= pos) ++b;
+    while (pos < x[w + 1]) {
+      while (start[b + 1] <= pos) ++b;   // skips requests without tokens
+      const long lo = pos - start[b], hi = std::min(x[w + 1], start[b + 1]) - start[b];
+      const long *cb = &cum[(size_t)b * (nchunks + 1)];
+      int c = 0;
+      for (long t = lo; t < hi;) {
+        while (cb[c + 1] <= t) ++c;
+        const long take = std::min({hi, cb[c + 1]}) - t;
+        for (long q = 0; q < take;) {
+          if (ranges == ss::kMaxChain) close();
+          if (ranges == 0) {
+            if (slot[b] >= ss::kNumSlots) return false;
+            ub = b;
+          }
+          const long n = std::min(take - q, pmax);
+          ss::Item it;
+          it.tok_begin = (int32_t)(off[(size_t)c * B + b] + (t - cb[c]) + q);
+          it.tok_count = (int32_t)n;
+          it.q_row0 = r->row_off[b];
+          it.n_cand = (uint8_t)r->n_cand[b];
+          it.chunk = (uint8_t)c;
+          it.slot = (uint8_t)slot[b];
+          it.flags = slot[b] >= r->slots_used[b] ? ss::kSlotFresh : 0;
+          plan->items.push_back(it);
+          ++ranges;
+          q += n;
+        }
+        t += take;
+      }
+      close();
+      pos = start[b] + hi;
+    }
+  }
+  plan->wg_first.push_back((uint32_t)plan->units());
+  for (int b = 0; b < B; ++b) plan->slots_after[b] = std::max(plan->slots_after[b], slot[b]);
   return true;
-}
-
-// Longest chains first (a short chain never delays the tail of the grid).
-void sort_chains(Chains *ch) {
-  std::vector<size_t> order(ch->size());
-  for (size_t c = 0; c < order.size(); ++c) order[c] = c;
-  std::vector<long> tok(order.size());
-  for (size_t c = 0; c < order.size(); ++c) tok[c] = ch->tokens(c);
-  std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return tok[a] > tok[b]; });
-  Chains out;
-  out.items.reserve(ch->items.size());
-  for (size_t c : order) {
-    out.items.insert(out.items.end(), ch->items.begin() + ch->start[c], ch->items.begin() + ch->start[c + 1]);
-    out.start.push_back((uint32_t)out.items.size());
-    out.kind.push_back(ch->kind[c]);
-  }
-  *ch = std::move(out);
 }
 
 ss_status plan_chunks(const ss_round *r, int nchunks, const int32_t *len, const std::vector<long> &tot,
                       Plan *plan) {
   long total = 0;
   for (long t : tot) total += t;
-  long piece;
+  long W;
   if (r->split_tokens > 0) {
-    piece = r->split_tokens;
+    W = (total + r->split_tokens - 1) / r->split_tokens;
   } else {
-    const long work = total * r->Hkv;
-    piece = (work + kTargetWorkgroups - 1) / kTargetWorkgroups;
-    // Ragged requests make units of unequal size; the longest-first order
-    // then needs several units per CU to balance the tail.
-    long lmin = -1, lmax = 0;
-    for (int b = 0; b < r->B; ++b) {
-      long L = 0;
-      for (int c = 0; c < nchunks; ++c) L += len[(size_t)c * r->B + b];
-      if (L == 0) continue;
-      lmin = lmin < 0 ? L : std::min(lmin, L);
-      lmax = std::max(lmax, L);
-    }
-    if (lmin > 0 && lmax != lmin) piece /= kRaggedSplit;
-    piece = std::min<long>(kMaxAutoPiece, std::max<long>(kMinPiece, align_up(piece, ss::kTile)));
+    W = std::max<long>(1, kTargetWorkgroups / r->Hkv);
+    W = std::min(W, std::max<long>(1, total / kMinPiece));
   }
+  W = std::max<long>(1, std::min<long>(W, total));
   const long pmax = max_piece_tokens(r);
-  piece = std::min(piece, pmax);
-  // every request must fit its pieces into the slots
-  while (!build_plan(r, nchunks, len, piece, plan)) {
-    if (piece >= pmax) return fail(SS_ERR_INVALID_ARGUMENT, "too many tokens per request for one history call");
-    piece = std::min(pmax, piece * 2);
+  // Fewer, larger shares until every request fits its units into the
+  // slots; more, smaller ones while a share would exceed one launch's unit
+  // or item table.
+  bool shrunk = false;
+  for (;;) {
+    if (!build_plan(r, nchunks, len, W, pmax, plan)) {
+      if (W == 1) return fail(SS_ERR_INVALID_ARGUMENT, "too many token ranges per request for one history call");
+      W = (W + 1) / 2;
+      shrunk = true;
+      continue;
+    }
+    bool fits = true;
+    for (size_t w = 0; w + 1 < plan->wg_first.size(); ++w)
+      if (plan->wg_first[w + 1] - plan->wg_first[w] > (uint32_t)ss::kMaxUnits ||
+          plan->unit_first[plan->wg_first[w + 1]] - plan->unit_first[plan->wg_first[w]] > (uint32_t)ss::kMaxItems)
+        fits = false;
+    if (fits) return SS_OK;
+    if (shrunk || W >= total) return fail(SS_ERR_INVALID_ARGUMENT, "history call too fragmented for one workgroup's tables");
+    W *= 2;
   }
-  sort_chains(&plan->chains);
-  return SS_OK;
 }
 
 ss::ChunkParams *base_params(const ss_round *r, int nchunks, const void *const *k, const void *const *v,
@@ -331,25 +340,33 @@ ss::ChunkParams *base_params(const ss_round *r, int nchunks, const void *const *
   return &p;
 }
 
-// Launch the chains of `ch` in batches of at most kMaxItems items and
-// kMaxUnits units with `launch(params)`.
+// Launch the workgroups of `plan` in batches of at most kMaxWgs workgroups,
+// kMaxUnits units and kMaxItems items with `launch(params)`.
 template <typename F>
-hipError_t launch_units(ss::ChunkParams *p, const Chains &ch, F launch) {
-  size_t c0 = 0;
-  while (c0 < ch.size()) {
-    size_t c1 = c0;
-    while (c1 < ch.size() && c1 - c0 < (size_t)ss::kMaxUnits &&
-           ch.start[c1 + 1] - ch.start[c0] <= (uint32_t)ss::kMaxItems)
-      ++c1;
-    const uint32_t i0 = ch.start[c0], n = ch.start[c1] - i0;
-    std::memcpy(p->items, ch.items.data() + i0, n * sizeof(ss::Item));
-    for (size_t c = c0; c < c1; ++c)
-      p->units[c - c0] = (ch.start[c] - i0) | ((ch.start[c + 1] - ch.start[c]) << 16) | ((uint32_t)ch.kind[c] << 24);
+hipError_t launch_units(ss::ChunkParams *p, const Plan &plan, F launch) {
+  const size_t W = plan.wg_first.size() - 1;
+  size_t w0 = 0;
+  while (w0 < W) {
+    const uint32_t u0 = plan.wg_first[w0];
+    const uint32_t i0 = plan.unit_first[u0];
+    size_t w1 = w0;
+    while (w1 < W && w1 - w0 < (size_t)ss::kMaxWgs && plan.wg_first[w1 + 1] - u0 <= (uint32_t)ss::kMaxUnits &&
+           plan.unit_first[plan.wg_first[w1 + 1]] - i0 <= (uint32_t)ss::kMaxItems)
+      ++w1;
+    if (w1 == w0) return hipErrorInvalidValue;   // one share over the table sizes (plan_chunks prevents it)
+    const uint32_t u1 = plan.wg_first[w1];
+    const uint32_t n = plan.unit_first[u1] - i0;
+    std::memcpy(p->items, plan.items.data() + i0, n * sizeof(ss::Item));
+    for (uint32_t u = u0; u < u1; ++u)
+      p->units[u - u0] = (plan.unit_first[u] - i0) | ((plan.unit_first[u + 1] - plan.unit_first[u]) << 16) |
+                         ((uint32_t)plan.kind[u] << 24);
+    for (size_t w = w0; w <= w1; ++w) p->wg_first[w - w0] = (uint16_t)(plan.wg_first[w] - u0);
     p->num_items = (int32_t)n;
-    p->num_units = (int32_t)(c1 - c0);
+    p->num_units = (int32_t)(u1 - u0);
+    p->num_wgs = (int32_t)(w1 - w0);
     const hipError_t e = launch(*p);
     if (e != hipSuccess) return e;
-    c0 = c1;
+    w0 = w1;
   }
   return hipSuccess;
 }
@@ -376,7 +393,7 @@ ss_status enqueue_history(ss_round *r, int nchunks, const void *const *k, const 
   ss_status s = plan_chunks(r, nchunks, len, tot, &plan);
   if (s != SS_OK) return s;
   ss::ChunkParams *p = base_params(r, nchunks, k, v, tot);
-  const hipError_t e = launch_units(p, plan.chains, [&](const ss::ChunkParams &q) { return ss::launch_chunk(q, stream); });
+  const hipError_t e = launch_units(p, plan, [&](const ss::ChunkParams &q) { return ss::launch_chunk(q, stream); });
   if (e != hipSuccess) return hip_fail(e, "history chunk kernel launch");
   r->slots_used = plan.slots_after;   // the slots written by this call are valid from now on
   return SS_OK;

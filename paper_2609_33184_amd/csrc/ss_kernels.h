@@ -9,7 +9,8 @@ namespace ss {
 constexpr int kHeadDim = 128;       // d
 constexpr int kNumSlots = 32;       // split slots of the running state per row
 constexpr int kMaxItems = 2048;     // work items per launch (kernel-argument list)
-constexpr int kMaxUnits = 1024;     // workgroup units per launch (x all KV heads)
+constexpr int kMaxUnits = 1024;     // units per launch (x all KV heads)
+constexpr int kMaxWgs = 1024;       // workgroups per KV head per launch
 constexpr int kMaxChain = 16;       // items (token ranges) per unit
 constexpr int kMaxChunks = 32;      // history chunks per launch
 constexpr int kTile = 32;           // history tokens per wave iteration
@@ -76,18 +77,22 @@ struct ChunkHeader {
   const uint16_t *v[kMaxChunks];
   uint64_t head_stride[kMaxChunks];   // elements between KV heads at the same token
   int32_t num_units;
+  int32_t num_wgs;      // workgroups per KV head (grid.y)
 };
 
-template <int MaxUnits, int MaxItems>
+template <int MaxUnits, int MaxItems, int MaxWgs>
 struct ChunkParamsT : ChunkHeader {
   static constexpr int kUnits = MaxUnits;
   static constexpr int kItems = MaxItems;
+  static constexpr int kWgs = MaxWgs;
   // unit u = items [units[u] & 0xffff, + ((units[u] >> 16) & 0xff)), 1..kMaxChain
   // items, attended by the body units[u] >> 24 (kUnitValu / kUnitMfma1 / kUnitMfma2)
   uint32_t units[MaxUnits];
+  // workgroup w (of every KV head) attends units [wg_first[w], wg_first[w + 1]) in order
+  uint16_t wg_first[MaxWgs + 1];
   Item items[MaxItems];
 };
-using ChunkParams = ChunkParamsT<kMaxUnits, kMaxItems>;   // what the host fills
+using ChunkParams = ChunkParamsT<kMaxUnits, kMaxItems, kMaxWgs>;   // what the host fills
 
 struct FinalHeader {
   const uint16_t *kc;   // bf16 candidate K [sum n_b, Hkv, d]
@@ -109,7 +114,7 @@ struct FinalParamsT : FinalHeader {
 using FinalParams = FinalParamsT<kMaxItems>;
 
 // Launch wrappers; return hipGetLastError() of the launch.
-// History units of every kind, grid (Hkv, num_units).
+// History units of every kind, grid (Hkv, num_wgs).
 hipError_t launch_chunk(const ChunkParams &p, hipStream_t s);
 // Speculative Frontier pass fused with the split-slot merge and O = a / l.
 hipError_t launch_finalize(const FinalParams &p, hipStream_t s);

@@ -89,14 +89,14 @@ __device__ __forceinline__ int global_row(const P &p, const Item &it, int g, int
 // fold the result into the item's slot of the running state (Eq. 14 again).
 // ---------------------------------------------------------------------------
 template <int ROWS, typename P>
-__device__ __forceinline__ void fold_into_slot(const P &p, const Item &it, int g, int M,
+__device__ __forceinline__ void fold_into_slot(const P &p, const Item &it, int g, int M, int tx,
                                                const float *aw, const float *mw, const float *lw) {
   // SEGS threads per row, SEGLEN (a multiple of 4) values each
   constexpr int SEGS = (256 / ROWS) < 32 ? (256 / ROWS) : 32;
   constexpr int SEGLEN = kHeadDim / SEGS;
   static_assert(SEGLEN % 4 == 0 && SEGS * ROWS <= 256, "fold layout");
-  const int r = threadIdx.x / SEGS;
-  const int seg = threadIdx.x % SEGS;
+  const int r = tx / SEGS;
+  const int seg = tx % SEGS;
   if (r >= M) return;
   float mwv[kWaves];
   float mstar = kNegInf;
@@ -250,9 +250,9 @@ __device__ __forceinline__ s16x4_t lds_read_tr16(const unsigned char *p) {
 }
 
 template <int RB, typename P>
-__device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i0, int nit) {
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
-  const int lane = threadIdx.x & 63;
+__device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i0, int nit, int tx) {
+  const int w = __builtin_amdgcn_readfirstlane(tx >> 6);   // wave-uniform
+  const int lane = tx & 63;
   const int lr = lane & 15;
   const int lq = lane >> 4;
   const Item it = p.items[i0];          // request, slot and flags of the whole chain
@@ -402,7 +402,7 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i
   u32x4_t qv[kQPerThread];
 #pragma unroll
   for (int e = 0; e < kQPerThread; ++e) {
-    const int c = threadIdx.x + 256 * e, r = c >> 4, ch = c & 15;
+    const int c = tx + 256 * e, r = c >> 4, ch = c & 15;
     const uint32_t qoff = r < M ? (uint32_t)global_row(p, it, g, r) * kRowBytes + 16 * ch : 0x80000000u;
     qv[e] = __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff, 0, 0);
   }
@@ -426,7 +426,7 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i
   load_kv(nx);
 #pragma unroll
   for (int e = 0; e < kQPerThread; ++e) {
-    const int c = threadIdx.x + 256 * e, r = c >> 4, ch = c & 15;
+    const int c = tx + 256 * e, r = c >> 4, ch = c & 15;
     *reinterpret_cast<u32x4_t *>(qs + r * kRowBytes + 16 * (ch ^ (r & 15))) = qv[e];
   }
   __syncthreads();
@@ -468,7 +468,7 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i
     }
   }
   __syncthreads();
-  fold_into_slot<RB * 16>(p, it, g, M, aw, mw, lw);
+  fold_into_slot<RB * 16>(p, it, g, M, tx, aw, mw, lw);
 }
 
 // ---------------------------------------------------------------------------
@@ -480,9 +480,9 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i
 // reduced over the 16 lanes of a DPP row.
 // ---------------------------------------------------------------------------
 template <int MAXR, typename P>
-__device__ __forceinline__ void valu_unit(const P &p, float *smem, int i0, int nit) {
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
-  const int lane = threadIdx.x & 63;
+__device__ __forceinline__ void valu_unit(const P &p, float *smem, int i0, int nit, int tx) {
+  const int w = __builtin_amdgcn_readfirstlane(tx >> 6);   // wave-uniform
+  const int lane = tx & 63;
   const int c = lane & 15;
   const int tg = lane >> 4;
   const Item it = p.items[i0];          // request, slot and flags of the whole chain
@@ -645,7 +645,7 @@ __device__ __forceinline__ void valu_unit(const P &p, float *smem, int i0, int n
     }
   }
   __syncthreads();
-  fold_into_slot<MAXR>(p, it, g, M, aw, mw, lw);
+  fold_into_slot<MAXR>(p, it, g, M, tx, aw, mw, lw);
 }
 
 constexpr int kValuLdsBytes = kWaves * kMaxValuRows * (kAwPitch + 2) * 4;
@@ -654,28 +654,38 @@ static_assert(MfmaLds<1>::kBytes <= kChunkLdsBytes, "LDS sizes");
 
 // ---------------------------------------------------------------------------
 // History kernel: one launch for every unit of a call.  Workgroup =
-// (kv head, unit) = (blockIdx.x, blockIdx.y); the unit's kind (from the
-// unit table) selects the body: MFMA with two or one 16-row blocks, or the
-// VALU path for <= 4 rows (when the round asks for it).  One launch keeps
-// the whole call in a single wave of workgroups whatever the mix of
-// candidate counts in the Cohort.  The heads are the fast grid dimension, so workgroups start in the unit
-// table's longest-first order across all heads, and with 8 KV heads the
-// round-robin placement gives every XCD one head of every unit (measured on
-// 64 ragged requests: 749-754 us with the unit-major grid, 731 us).
+// (kv head, w) = (blockIdx.x, blockIdx.y) attends the units of its list in
+// order (the host gives every workgroup an equal share of the call's
+// tokens, which may span several requests); each unit's kind selects the
+// body: MFMA with two or one 16-row blocks, or the VALU path for <= 4 rows
+// (when the round asks for it).  The heads are the fast grid dimension: with
+// 8 KV heads the round-robin placement gives every XCD one head of every
+// workgroup's share.
 // ---------------------------------------------------------------------------
 template <typename P>
 __global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[kChunkLdsBytes];
-  const uint32_t unit = p.units[blockIdx.y];
-  const int i0 = unit & 0xffff;
-  const int nit = (unit >> 16) & 0xff;
-  const int kind = unit >> 24;
-  if (kind == kUnitMfma2)
-    mfma_unit<2>(p, smem, i0, nit);
-  else if (kind == kUnitMfma1)
-    mfma_unit<1>(p, smem, i0, nit);
-  else
-    valu_unit<kMaxValuRows>(p, reinterpret_cast<float *>(smem), i0, nit);
+  const int u0 = p.wg_first[blockIdx.y];
+  const int u1 = p.wg_first[blockIdx.y + 1];
+  for (int u = u0; u < u1; ++u) {
+    if (u != u0) __syncthreads();   // the previous unit's fold has read the LDS this unit restages
+    // The bodies derive their per-lane addresses from tx.  Passing it
+    // through an empty asm each unit keeps the compiler from computing
+    // them once before the loop and holding all three bodies' worth live
+    // across it (that spilled 14 registers and cost 6% on one-unit calls).
+    int tx = threadIdx.x;
+    asm volatile("" : "+v"(tx));
+    const uint32_t unit = p.units[u];
+    const int i0 = unit & 0xffff;
+    const int nit = (unit >> 16) & 0xff;
+    const int kind = unit >> 24;
+    if (kind == kUnitMfma2)
+      mfma_unit<2>(p, smem, i0, nit, tx);
+    else if (kind == kUnitMfma1)
+      mfma_unit<1>(p, smem, i0, nit, tx);
+    else
+      valu_unit<kMaxValuRows>(p, reinterpret_cast<float *>(smem), i0, nit, tx);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -792,10 +802,10 @@ __global__ void __launch_bounds__(256) finalize_kernel(const P p) {
 namespace {
 
 // Table capacities of the launches: a Cohort's whole history call usually
-// fits the small class (config 3: 32 units, 128 items), large ragged
-// batches the medium one.
-using ChunkSmall = ChunkParamsT<64, 256>;
-using ChunkMedium = ChunkParamsT<256, 1024>;
+// fits the small class (config 3: 32 workgroups per KV head, 32 units, 128
+// items), large ragged batches the medium one.
+using ChunkSmall = ChunkParamsT<128, 256, 128>;
+using ChunkMedium = ChunkParamsT<512, 1024, 256>;
 using FinalSmall = FinalParamsT<64>;
 
 template <typename D>
@@ -803,19 +813,21 @@ hipError_t launch_chunk_as(const ChunkParams &p, hipStream_t s) {
   static thread_local D d;
   static_cast<ChunkHeader &>(d) = p;
   std::memcpy(d.units, p.units, sizeof(uint32_t) * p.num_units);
+  std::memcpy(d.wg_first, p.wg_first, sizeof(uint16_t) * (p.num_wgs + 1));
   std::memcpy(d.items, p.items, sizeof(Item) * p.num_items);
-  hipLaunchKernelGGL(chunk_attn<D>, dim3(p.Hkv, p.num_units), dim3(256), 0, s, d);
+  hipLaunchKernelGGL(chunk_attn<D>, dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, d);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_chunk(const ChunkParams &p, hipStream_t s) {
-  if (p.num_units <= ChunkSmall::kUnits && p.num_items <= ChunkSmall::kItems)
-    return launch_chunk_as<ChunkSmall>(p, s);
-  if (p.num_units <= ChunkMedium::kUnits && p.num_items <= ChunkMedium::kItems)
-    return launch_chunk_as<ChunkMedium>(p, s);
-  hipLaunchKernelGGL(chunk_attn<ChunkParams>, dim3(p.Hkv, p.num_units), dim3(256), 0, s, p);
+  auto fits = [&](int units, int items, int wgs) {
+    return p.num_units <= units && p.num_items <= items && p.num_wgs <= wgs;
+  };
+  if (fits(ChunkSmall::kUnits, ChunkSmall::kItems, ChunkSmall::kWgs)) return launch_chunk_as<ChunkSmall>(p, s);
+  if (fits(ChunkMedium::kUnits, ChunkMedium::kItems, ChunkMedium::kWgs)) return launch_chunk_as<ChunkMedium>(p, s);
+  hipLaunchKernelGGL(chunk_attn<ChunkParams>, dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

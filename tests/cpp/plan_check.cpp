@@ -1,7 +1,9 @@
 // CPU check of the history-call planner together with the chunk kernels' tile
 // traversal: every token of every request is visited exactly once per KV
 // head, every buffer resource stays inside its chunk, chains are
-// single-request and single-slot, slots and fresh flags are consistent.
+// single-request and single-slot, slots and fresh flags are consistent, the
+// workgroup lists cover every unit once, and every workgroup's share of the
+// call is within one tile of the mean.
 // The kernel launchers are stubs that record the launch tables.
 #include "ss_kernels.h"
 #include "specstream.h"
@@ -14,7 +16,7 @@
 #include <set>
 
 namespace {
-struct Rec { std::vector<ss::Item> items; std::vector<uint32_t> units; int kind; };
+struct Rec { std::vector<ss::Item> items; std::vector<uint32_t> units; std::vector<uint16_t> wg_first; int kind; };
 std::vector<Rec> g_recs;
 const ss::ChunkParams *g_last = nullptr;
 }
@@ -24,6 +26,8 @@ static void rec(const ChunkParams &p, int kind) {
   Rec r;
   r.items.assign(p.items, p.items + p.num_items);
   r.units.assign(p.units, p.units + p.num_units);
+  r.wg_first.assign(p.wg_first, p.wg_first + p.num_wgs + 1);
+  if (p.num_wgs < 1 || p.num_wgs > kMaxWgs) { printf("bad workgroup count\n"); exit(1); }
   r.kind = kind;
   if (p.num_units < 1 || p.num_units > kMaxUnits || p.num_items < 1 || p.num_items > kMaxItems) { printf("bad counts\n"); exit(1); }
   g_recs.push_back(r);
@@ -59,6 +63,23 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
   const int G = Hq / Hkv;
   std::vector<int> off_rows(B, 0);
   for (int b = 1; b < B; ++b) off_rows[b] = off_rows[b - 1] + ncand[b - 1];
+  // workgroup lists: cover every unit once, in order; shares are equal
+  long total = 0, wgs = 0, max_share = 0;
+  for (auto &row : lens) for (int x : row) total += x;
+  for (auto &rc : g_recs) {
+    CHECK(rc.wg_first.front() == 0 && rc.wg_first.back() == rc.units.size(), "workgroup table ends");
+    for (size_t w = 0; w + 1 < rc.wg_first.size(); ++w) {
+      CHECK(rc.wg_first[w] <= rc.wg_first[w + 1], "workgroup table order");
+      long share = 0;
+      for (int u = rc.wg_first[w]; u < rc.wg_first[w + 1]; ++u) {
+        const int i0 = rc.units[u] & 0xffff, nit = (rc.units[u] >> 16) & 0xff;
+        for (int k = 0; k < nit; ++k) share += rc.items[i0 + k].tok_count;
+      }
+      max_share = std::max(max_share, share);
+      ++wgs;
+    }
+  }
+  if (total >= 32 * wgs) CHECK(max_share <= (total + wgs - 1) / wgs + 31, "share %ld > mean %ld + a tile", max_share, total / wgs);
   for (auto &rc : g_recs) {
     for (size_t u = 0; u < rc.units.size(); ++u) {
       const int i0 = rc.units[u] & 0xffff, nit = (rc.units[u] >> 16) & 0xff, kind = rc.units[u] >> 24;
