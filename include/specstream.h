@@ -79,8 +79,11 @@ typedef struct {
   float softmax_scale;      /* sigma > 0, finite; 1/sqrt(d) in the paper       */
   const int32_t *num_cand;  /* host [B]: n_b = k_b + 1, 1 <= n_b <= 8, copied  */
   int32_t max_chunk_tokens; /* >= 1: bound on sum_b len_b of one history call  */
-  int32_t split_tokens;     /* tokens per workgroup piece; 0 = automatic;
-                               else a multiple of 32                           */
+  int32_t split_tokens;     /* tokens per workgroup share: a history call's
+                               tokens (all requests, in request order) are
+                               split into equal shares of about this many,
+                               one per workgroup and KV head; 0 = automatic
+                               (one workgroup per CU); else a multiple of 32  */
   int32_t mfma_min_rows;    /* rows per KV head (n_b * G) from which the bf16
                                MFMA path is used; fewer (at most 4) use the
                                fp32 VALU path.  0 = default (1: always MFMA,
