@@ -331,6 +331,9 @@ def ablation(torch, H, ss, W, stream, layout: int):
             host = H.HostHistory(w, kv_layout=layout)
             b = H.RoundBuffers(w, kv_layout=layout)
             res = {}
+
+            def vofs(j):   # bytes from a chunk's K to its V in a staging buffer
+                return 2 * w.head_dim if layout == ss.SS_KV_HEAD_MAJOR_KV else host.sizes[j] // 2
             # K1: restore everything, then one batched attention call
             dev = [torch.empty(host.sizes[j], dtype=torch.uint8, device="cuda") for j in range(w.num_chunks)]
             copy = torch.cuda.Stream()
@@ -342,7 +345,7 @@ def ablation(torch, H, ss, W, stream, layout: int):
                                            None, done if j == w.num_chunks - 1 else None)
                     r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream.cuda_stream)
                     try:
-                        half = [host.sizes[j] // 2 for j in range(w.num_chunks)]
+                        half = [vofs(j) for j in range(w.num_chunks)]
                         ss.ss_attend_history_chunks(r, [dev[j].data_ptr() for j in range(w.num_chunks)],
                                                     [dev[j].data_ptr() + half[j] for j in range(w.num_chunks)],
                                                     [w.chunk_lens(j) for j in range(w.num_chunks)], done, None,
@@ -359,7 +362,7 @@ def ablation(torch, H, ss, W, stream, layout: int):
                         r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream.cuda_stream)
                         try:
                             for j in range(w.num_chunks):
-                                half = host.sizes[j] // 2
+                                half = vofs(j)
                                 ss.ss_upload_chunk(slot.data_ptr(), host.chunk_ptr(j), host.sizes[j], copy.cuda_stream,
                                                    free if j else None, ready)
                                 ss.ss_attend_history_chunk(r, slot.data_ptr(), slot.data_ptr() + half, w.chunk_lens(j),
@@ -419,8 +422,9 @@ def main() -> int:
     ap.add_argument("--batch", type=int, default=0,
                     help="history chunks per ss_attend_history_chunks call in the timed round "
                          "(0 = all resident chunks in one call, 1 = one call per chunk)")
-    ap.add_argument("--kv-layout", choices=["token", "head"], default="head",
-                    help="history chunk layout: token-major [tok][Hkv][d] or head-major [Hkv][tok][d]")
+    ap.add_argument("--kv-layout", choices=["token", "head", "head-kv"], default="head",
+                    help="history chunk layout: token-major [tok][Hkv][d], head-major [Hkv][tok][d] or "
+                         "head-major with each token's K and V rows adjacent [Hkv][tok][2][d]")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-streamed", action="store_true")
     ap.add_argument("--cpu-sample-requests", type=int, default=6)
@@ -465,7 +469,7 @@ def main() -> int:
         w = W.custom(w.hist_len, [args.num_cand] * w.B, num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads,
                      head_dim=w.head_dim, chunk_tokens=w.chunk_tokens, cfg_id=args.config)
     log(f"bench: config {args.config} ({w.name}): generating inputs on the GPU")
-    layout = ss.SS_KV_HEAD_MAJOR if args.kv_layout == "head" else ss.SS_KV_TOKEN_MAJOR
+    layout = {"token": ss.SS_KV_TOKEN_MAJOR, "head": ss.SS_KV_HEAD_MAJOR, "head-kv": ss.SS_KV_HEAD_MAJOR_KV}[args.kv_layout]
     b = H.RoundBuffers(w, split_tokens=args.split_tokens, kv_layout=layout, mfma_min_rows=args.mfma_min_rows)
     chunks = H.hbm_history(w, kv_layout=layout)
     stream = torch.cuda.Stream()
@@ -532,7 +536,7 @@ def main() -> int:
             "workload": f"config {args.config}: {w.B} requests x {w.hist_len[0] if len(set(w.hist_len)) == 1 else 'ragged'} "
                         f"history tokens, {w.num_q_heads}q/{w.num_kv_heads}kv heads, d={w.head_dim}, "
                         f"{w.num_chunks} chunks of {w.chunk_tokens}, {w.num_cand[0] if len(set(w.num_cand)) == 1 else 'ragged'} "
-                        f"candidate queries, history resident in HBM ({args.kv_layout}-major chunks)",
+                        f"candidate queries, history resident in HBM ({args.kv_layout} chunk layout)",
             "round_latency_ms": round(step_s * 1e3, 4),
             "round_latency_us_p10_p50_p90": [round(pct(per_round, q) * 1e6, 2) for q in (0.1, 0.5, 0.9)],
             "chunks_per_history_call": batch,

@@ -90,15 +90,21 @@ typedef struct {
                                the faster body at every row count); 2..5 =
                                VALU below that many rows; range 0..5           */
   int32_t kv_layout;        /* layout of history chunks: SS_KV_TOKEN_MAJOR
-                               [sum_b len_b][Hkv][d] or SS_KV_HEAD_MAJOR
-                               [Hkv][sum_b len_b][d]                           */
+                               [sum_b len_b][Hkv][d], SS_KV_HEAD_MAJOR
+                               [Hkv][sum_b len_b][d] or SS_KV_HEAD_MAJOR_KV
+                               [Hkv][sum_b len_b][2][d] (K and V rows of a
+                               token adjacent)                                 */
 } ss_round_desc;
 
-/* History chunk layouts (ss_round_desc.kv_layout).  In both, request b's
+/* History chunk layouts (ss_round_desc.kv_layout).  In all, request b's
  * len_b tokens follow request b-1's; head-major keeps each KV head's tokens
- * contiguous (one contiguous stream per workgroup). */
+ * contiguous (one contiguous stream per workgroup for K and one for V).
+ * SS_KV_HEAD_MAJOR_KV keeps K and V of one chunk in one buffer, each token's
+ * K row followed by its V row, so a workgroup reads a single contiguous
+ * stream; the chunk's v pointer must then be its k pointer + d elements. */
 #define SS_KV_TOKEN_MAJOR 0
 #define SS_KV_HEAD_MAJOR 1
+#define SS_KV_HEAD_MAJOR_KV 2
 
 /* Bytes of device workspace a round with this descriptor needs (fp32
  * online-softmax states of every query row, per split slot).  0 if the
@@ -184,7 +190,8 @@ ss_status ss_pipeline_create(ss_pipeline **out, void *staging0, void *staging1, 
  *   copy_stream: wait free[s]; copy host_kv -> slot s; record ready[s]
  *   stream:      wait ready[s]; ss_attend_history_chunk; record free[s]
  * host_kv: pinned host bf16, the chunk's K then its V, each in the round's
- * kv_layout ([sum_b len_b][Hkv][d] or [Hkv][sum_b len_b][d]), contiguous;
+ * kv_layout ([sum_b len_b][Hkv][d] or [Hkv][sum_b len_b][d]), contiguous
+ * (SS_KV_HEAD_MAJOR_KV: the chunk's one [Hkv][sum_b len_b][2][d] buffer);
  * len as in ss_attend_history_chunk.  The chunk may belong
  * to any round (e.g. the next layer), so transfers run ahead across layer
  * boundaries. */
@@ -196,7 +203,8 @@ ss_status ss_pipeline_attend_chunk(ss_pipeline *p, ss_round *r, const void *host
  * upload num_chunks adjacent history chunks into the next staging slot with
  * one copy and attend them with one launch, as ss_attend_history_chunks
  * does.  host_kv: pinned host memory holding chunk 0's K, chunk 0's V, chunk
- * 1's K, ... contiguously (each in the round's kv_layout); len: host
+ * 1's K, ... contiguously (each in the round's kv_layout; with
+ * SS_KV_HEAD_MAJOR_KV each chunk's one K-and-V buffer); len: host
  * [num_chunks][B]; 1 <= num_chunks <= 32; the batch must fit slot_bytes. */
 ss_status ss_pipeline_attend_chunks(ss_pipeline *p, ss_round *r, int32_t num_chunks, const void *host_kv,
                                     const int32_t *len, hipStream_t stream);

@@ -82,8 +82,8 @@ ss_status validate_desc(const ss_round_desc *d) {
     return fail(SS_ERR_INVALID_ARGUMENT, "split_tokens must be 0 or a positive multiple of %d", ss::kTile);
   if (d->mfma_min_rows < 0 || d->mfma_min_rows > ss::kMaxValuRows + 1)
     return fail(SS_ERR_INVALID_ARGUMENT, "mfma_min_rows must be in [0, %d]", ss::kMaxValuRows + 1);
-  if (d->kv_layout != SS_KV_TOKEN_MAJOR && d->kv_layout != SS_KV_HEAD_MAJOR)
-    return fail(SS_ERR_INVALID_ARGUMENT, "kv_layout must be SS_KV_TOKEN_MAJOR or SS_KV_HEAD_MAJOR");
+  if (d->kv_layout != SS_KV_TOKEN_MAJOR && d->kv_layout != SS_KV_HEAD_MAJOR && d->kv_layout != SS_KV_HEAD_MAJOR_KV)
+    return fail(SS_ERR_INVALID_ARGUMENT, "kv_layout must be SS_KV_TOKEN_MAJOR, SS_KV_HEAD_MAJOR or SS_KV_HEAD_MAJOR_KV");
   const int G = d->num_q_heads / d->num_kv_heads;
   long rows = 0;
   for (int b = 0; b < d->num_requests; ++b) {
@@ -141,9 +141,18 @@ ss_status check_round(const ss_round *r) {
   return SS_OK;
 }
 
+// Elements between consecutive tokens of one KV head in a chunk.
+uint32_t tok_stride(const ss_round *r) {
+  switch (r->kv_layout) {
+    case SS_KV_TOKEN_MAJOR: return (uint32_t)(r->Hkv * ss::kHeadDim);
+    case SS_KV_HEAD_MAJOR_KV: return 2 * ss::kHeadDim;
+    default: return ss::kHeadDim;
+  }
+}
+
 long max_piece_tokens(const ss_round *r) {
   // an item must stay below 2^31 bytes of one KV head (32-bit buffer offsets)
-  const long per_tok = r->kv_layout == SS_KV_TOKEN_MAJOR ? (long)r->Hkv * 2 * ss::kHeadDim : 2 * ss::kHeadDim;
+  const long per_tok = 2 * (long)tok_stride(r);
   return ((1L << 31) - 1024) / per_tok / ss::kTile * ss::kTile;
 }
 
@@ -170,6 +179,10 @@ ss_status check_history_args(const ss_round *r, int nchunks, const void *const *
     if (t > 0 && (k == nullptr || v == nullptr || k[c] == nullptr || v[c] == nullptr || !aligned(k[c], 16) ||
                   !aligned(v[c], 16)))
       return fail(SS_ERR_INVALID_ARGUMENT, "chunk %d: k and v must be non-null and 16-byte aligned", c);
+    if (t > 0 && r->kv_layout == SS_KV_HEAD_MAJOR_KV &&
+        static_cast<const char *>(v[c]) != static_cast<const char *>(k[c]) + ss::kHeadDim * 2)
+      return fail(SS_ERR_INVALID_ARGUMENT, "chunk %d: with SS_KV_HEAD_MAJOR_KV, v must be k + %d elements", c,
+                  ss::kHeadDim);
     (*tot)[c] = t;
   }
   return SS_OK;
@@ -329,11 +342,11 @@ ss::ChunkParams *base_params(const ss_round *r, int nchunks, const void *const *
   p.Hkv = r->Hkv;
   p.G = r->G;
   p.scale_log2 = r->scale * 1.4426950408889634f;
-  p.tok_stride = r->kv_layout == SS_KV_TOKEN_MAJOR ? (uint32_t)(r->Hkv * ss::kHeadDim) : ss::kHeadDim;
+  p.tok_stride = tok_stride(r);
   for (int c = 0; c < nchunks; ++c) {
     p.k[c] = static_cast<const uint16_t *>(k[c]);
     p.v[c] = static_cast<const uint16_t *>(v[c]);
-    p.head_stride[c] = r->kv_layout == SS_KV_TOKEN_MAJOR ? (uint64_t)ss::kHeadDim : (uint64_t)tot[c] * ss::kHeadDim;
+    p.head_stride[c] = r->kv_layout == SS_KV_TOKEN_MAJOR ? (uint64_t)ss::kHeadDim : (uint64_t)tot[c] * tok_stride(r);
   }
   p.num_items = 0;
   p.num_units = 0;
@@ -599,7 +612,8 @@ ss_status ss_pipeline_attend_chunks(ss_pipeline *p, ss_round *r, int32_t num_chu
   if (num_chunks < 1 || num_chunks > ss::kMaxChunks)
     return fail(SS_ERR_INVALID_ARGUMENT, "num_chunks = %d outside [1, %d]", num_chunks, ss::kMaxChunks);
   if (len == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "len is null");
-  // chunk c occupies [off[c], off[c] + 2 * half[c]) of the slot: its K, then its V
+  // chunk c occupies [off[c], off[c] + 2 * half[c]) of the slot: its K, then
+  // its V (SS_KV_HEAD_MAJOR_KV: one buffer of K and V rows)
   const int sl = p->next;
   std::vector<const void *> kk(num_chunks), vv(num_chunks);
   size_t bytes = 0;
@@ -608,7 +622,7 @@ ss_status ss_pipeline_attend_chunks(ss_pipeline *p, ss_round *r, int32_t num_chu
     for (int b = 0; b < r->B; ++b) total += std::max<int32_t>(0, len[(size_t)c * r->B + b]);
     const size_t half = (size_t)total * r->Hkv * ss::kHeadDim * 2;
     kk[c] = p->slot[sl] + bytes;
-    vv[c] = p->slot[sl] + bytes + half;
+    vv[c] = p->slot[sl] + bytes + (r->kv_layout == SS_KV_HEAD_MAJOR_KV ? ss::kHeadDim * 2 : half);
     bytes += 2 * half;
   }
   std::vector<long> tot;

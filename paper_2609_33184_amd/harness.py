@@ -49,8 +49,8 @@ def hbm_history(w: Workload, layer: int = 0, device="cuda", kv_layout: int = ss.
                 ) -> List[Tuple[torch.Tensor, torch.Tensor]]:
     """Every history chunk resident in device memory: [(k_j, v_j)] in the
     given chunk layout."""
-    hm = kv_layout == ss.SS_KV_HEAD_MAJOR
-    return [w.chunk_kv(j, layer, device, head_major=hm) for j in range(w.num_chunks)]
+    return [w.chunk_kv(j, layer, device, head_major=kv_layout == ss.SS_KV_HEAD_MAJOR,
+                       kv_interleaved=kv_layout == ss.SS_KV_HEAD_MAJOR_KV) for j in range(w.num_chunks)]
 
 
 def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor]], stream: int,
@@ -93,12 +93,13 @@ def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor
 
 class HostHistory:
     """One layer's history in pinned host memory, chunk j as its K then its V
-    (each in the round's chunk layout), for streaming through the two-slot
-    pipeline."""
+    (each in the round's chunk layout; with the interleaved layout the chunk's
+    one K-and-V buffer), for streaming through the two-slot pipeline."""
 
     def __init__(self, w: Workload, layer: int = 0, gen_device="cuda", kv_layout: int = ss.SS_KV_TOKEN_MAJOR):
         self.w = w
         hm = kv_layout == ss.SS_KV_HEAD_MAJOR
+        il = kv_layout == ss.SS_KV_HEAD_MAJOR_KV
         tb = w.num_kv_heads * w.head_dim * BF16_BYTES
         self.sizes = [2 * sum(w.chunk_lens(j)) * tb for j in range(w.num_chunks)]
         self.offsets = []
@@ -111,11 +112,15 @@ class HostHistory:
         for j in range(w.num_chunks):
             if self.sizes[j] == 0:
                 continue
-            k, v = w.chunk_kv(j, layer, gen_device, head_major=hm)
+            k, v = w.chunk_kv(j, layer, gen_device, head_major=hm, kv_interleaved=il)
             half = self.sizes[j] // 2
             o = self.offsets[j]
-            self.buf[o:o + half].copy_(k.view(-1).view(torch.uint8).cpu())
-            self.buf[o + half:o + 2 * half].copy_(v.view(-1).view(torch.uint8).cpu())
+            if il:      # one buffer: the views' base holds K and V rows
+                kv = torch.as_strided(k, (self.sizes[j] // BF16_BYTES,), (1,))
+                self.buf[o:o + 2 * half].copy_(kv.view(torch.uint8).cpu())
+            else:
+                self.buf[o:o + half].copy_(k.view(-1).view(torch.uint8).cpu())
+                self.buf[o + half:o + 2 * half].copy_(v.view(-1).view(torch.uint8).cpu())
             del k, v
 
     def chunk_ptr(self, j: int) -> int:

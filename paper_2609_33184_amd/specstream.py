@@ -26,6 +26,7 @@ SS_ERR_HIP = -6
 
 SS_KV_TOKEN_MAJOR = 0   # history chunk [sum len][Hkv][d]
 SS_KV_HEAD_MAJOR = 1    # history chunk [Hkv][sum len][d]
+SS_KV_HEAD_MAJOR_KV = 2  # history chunk [Hkv][sum len][2][d]: K and V rows of a token adjacent (v = k + d)
 
 EXPORTED = (
     "ss_round_workspace_bytes", "ss_round_init", "ss_upload_chunk", "ss_attend_history_chunk",

@@ -333,10 +333,16 @@ class Workload:
     def v_cand_all(self, layer: int = 0, device="cpu") -> torch.Tensor:
         return torch.cat([self.v_cand(b, layer=layer, device=device) for b in range(self.B)], 0)
 
-    def chunk_kv(self, j: int, layer: int = 0, device="cpu", out_k=None, out_v=None, head_major: bool = False
-                 ) -> Tuple[torch.Tensor, torch.Tensor]:
+    def chunk_kv(self, j: int, layer: int = 0, device="cpu", out_k=None, out_v=None, head_major: bool = False,
+                 kv_interleaved: bool = False) -> Tuple[torch.Tensor, torch.Tensor]:
         """History chunk j packed in request order: [sum_b len_bj, Hkv, d] each
-        (token-major), or [Hkv, sum_b len_bj, d] with ``head_major``."""
+        (token-major), or [Hkv, sum_b len_bj, d] with ``head_major``.  With
+        ``kv_interleaved`` both live in one [Hkv, sum_b len_bj, 2, d] buffer
+        (a token's K row, then its V row) and K, V are views of it."""
+        if kv_interleaved:
+            k, v = self.chunk_kv(j, layer, device)
+            kv = torch.stack((k.transpose(0, 1), v.transpose(0, 1)), dim=2).contiguous()
+            return kv[:, :, 0], kv[:, :, 1]
         if head_major:
             k, v = self.chunk_kv(j, layer, device)
             return k.transpose(0, 1).contiguous(), v.transpose(0, 1).contiguous()

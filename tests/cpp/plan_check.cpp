@@ -51,7 +51,10 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
   for (int c = 0; c < nch; ++c) for (int b = 0; b < B; ++b) { flat.push_back(lens[c][b]); tot[c] += lens[c][b]; }
   std::vector<const void *> kp(nch), vp(nch);
   // fake aligned chunk pointers; never dereferenced
-  for (int c = 0; c < nch; ++c) { kp[c] = (const void *)(uintptr_t)(0x100000000ull * (c + 1)); vp[c] = (const void *)(uintptr_t)(0x100000000ull * (c + 1) + 0x80000000ull); }
+  for (int c = 0; c < nch; ++c) {
+    kp[c] = (const void *)(uintptr_t)(0x100000000ull * (c + 1));
+    vp[c] = (const void *)(uintptr_t)(0x100000000ull * (c + 1) + (layout == SS_KV_HEAD_MAJOR_KV ? 256 : 0x80000000ull));
+  }
   g_recs.clear();
   ss_status s = ss_attend_history_chunks(r, nch, kp.data(), vp.data(), flat.data(), nullptr, nullptr, nullptr);
   CHECK(s == SS_OK, "status %d: %s", s, ss_last_error());
@@ -105,12 +108,15 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
         for (int bb = 0; bb < b; ++bb) ofs += lens[ik.chunk][bb];
         CHECK(ik.tok_begin >= ofs && ik.tok_begin + ik.tok_count <= ofs + lens[ik.chunk][b], "item outside request range");
         // buffer resource bounds for every head: [first, first + nrec) inside the chunk
-        const long stride = layout == SS_KV_TOKEN_MAJOR ? (long)Hkv * 128 : 128;
-        const long hstride = layout == SS_KV_TOKEN_MAJOR ? 128 : tot[ik.chunk] * 128;
+        const bool il = layout == SS_KV_HEAD_MAJOR_KV;
+        const long stride = layout == SS_KV_TOKEN_MAJOR ? (long)Hkv * 128 : il ? 256 : 128;
+        const long hstride = layout == SS_KV_TOKEN_MAJOR ? 128 : tot[ik.chunk] * stride;
+        const long bytes = tot[ik.chunk] * Hkv * 256 * (il ? 2 : 1);   // the buffer K (and V) offsets index
         for (int g = 0; g < Hkv; ++g) {
           const long first = (long)ik.tok_begin * stride + (long)g * hstride;
           const long nrec = (long)(ik.tok_count - 1) * stride * 2 + 256;
-          CHECK(first * 2 + nrec <= tot[ik.chunk] * Hkv * 256, "rsrc past chunk");
+          CHECK(first * 2 + nrec <= bytes, "K rsrc past chunk");
+          CHECK(first * 2 + (il ? 256 : 0) + nrec <= bytes, "V rsrc past chunk");
           CHECK(nrec < (1L << 31), "nrec 32-bit");
         }
       }
@@ -178,7 +184,7 @@ static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> 
 
 int main() {
   std::mt19937 rng(7);
-  for (int layout : {SS_KV_TOKEN_MAJOR, SS_KV_HEAD_MAJOR}) {
+  for (int layout : {SS_KV_TOKEN_MAJOR, SS_KV_HEAD_MAJOR, SS_KV_HEAD_MAJOR_KV}) {
     scenario("config1 per-chunk", 1, 8, 2, {5}, {4096}, 1024, 0, layout, 1);
     scenario("config1 split 32", 1, 8, 2, {5}, {4096}, 1024, 32, layout, 1);
     scenario("config1 split 96", 1, 8, 2, {5}, {4096}, 1024, 96, layout, 1);

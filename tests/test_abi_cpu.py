@@ -80,7 +80,7 @@ def test_workspace_bytes_and_descriptor_validation(lib):
         (ss.make_desc([4], 8, 2, softmax_scale=float("inf")), "softmax_scale"),
         (ss.make_desc([4], 8, 2, split_tokens=48), "split_tokens"),
         (ss.make_desc([4], 8, 2, mfma_min_rows=6), "mfma_min_rows"),
-        (ss.make_desc([4], 8, 2, kv_layout=2), "kv_layout"),
+        (ss.make_desc([4], 8, 2, kv_layout=3), "kv_layout"),
         (ss.make_desc([4], 8, 2, max_chunk_tokens=0), "max_chunk_tokens"),
     ]
     for desc, word in bad:
@@ -129,6 +129,14 @@ def test_call_order_and_chunk_arguments(lib):
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_history_chunk, r, K + 2, V, [10, 3])  # misaligned
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_history_chunk, r, 0, V, [10, 3])
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_history_chunks, r, [K] * 33, [V] * 33, [[1, 1]] * 33)
+        # the K-and-V layout takes v = k + d elements
+        d2 = ss.make_desc([5, 2], 8, 2, max_chunk_tokens=1024, kv_layout=ss.SS_KV_HEAD_MAJOR_KV)
+        r2 = ss.ss_round_init(d2, FAKE_Q, FAKE_WS, ss.ss_round_workspace_bytes(d2))
+        try:
+            expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_history_chunk, r2, K, V, [10, 3])
+            expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_history_chunk, r2, K, K + 128, [10, 3])
+        finally:
+            ss.ss_round_destroy(r2)
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_local_candidates, r, 0, V)
         ss.ss_attend_local_candidates(r, K, V)                                     # records pointers only
         expect(ss.SS_ERR_BAD_STATE, ss.ss_attend_local_candidates, r, K, V)

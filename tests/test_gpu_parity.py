@@ -28,8 +28,8 @@ def stream():
     torch.cuda.synchronize()
 
 
-LAYOUTS = [ss.SS_KV_TOKEN_MAJOR, ss.SS_KV_HEAD_MAJOR]
-LAYOUT_IDS = ["token_major", "head_major"]
+LAYOUTS = [ss.SS_KV_TOKEN_MAJOR, ss.SS_KV_HEAD_MAJOR, ss.SS_KV_HEAD_MAJOR_KV]
+LAYOUT_IDS = ["token_major", "head_major", "head_major_kv"]
 
 
 def _run(w, stream, kv_layout=ss.SS_KV_TOKEN_MAJOR, **kw):
