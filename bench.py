@@ -138,11 +138,14 @@ def cpu_baseline(w, chunks, sample_requests):
                     vs.append(v[off:off + lens[b]].cpu())
         host.append((bf16_bits(w.q(b)), bf16_bits(torch.cat(ks)), bf16_bits(torch.cat(vs)),
                      bf16_bits(w.k_cand(b)), bf16_bits(w.v_cand(b))))
+    c0 = os.times()
     t0 = time.perf_counter()
     for (q, kh, vh, kc, vc) in host:
         oracle.verify_attention([bf16_bits_to_f64(q)], [bf16_bits_to_f64(kh)], [bf16_bits_to_f64(vh)],
                                 [bf16_bits_to_f64(kc)], [bf16_bits_to_f64(vc)], scale=w.softmax_scale)
     dt = time.perf_counter() - t0
+    c1 = os.times()
+    cpu_s = (c1.user - c0.user) + (c1.system - c0.system)   # every thread of this process
     nbytes = sum((w.hist_len[b] + w.num_cand[b]) * w.token_bytes() for b in sample_requests)
     cores = len(os.sched_getaffinity(0))
     # the same oracle limited to one BLAS thread, on the first sampled request
@@ -160,7 +163,9 @@ def cpu_baseline(w, chunks, sample_requests):
                "cores": 1, "seconds": round(d1, 3), "sample": f"request {b0} only"}
     except Exception:  # pragma: no cover
         one = None
-    return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": blas_threads or cores,
+    # cores: the threads the oracle kept busy on average (CPU time / wall time)
+    return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": max(1, round(cpu_s / dt)),
+            "cpu_seconds": round(cpu_s, 2), "blas_threads": blas_threads,
             "host_cores_available": cores, "kind": "oracle",
             "seconds": round(dt, 3), "one_thread": one,
             "sample": f"fp64 numpy oracle (direct masked softmax) over {len(sample_requests)} of {w.B} requests "
@@ -427,7 +432,8 @@ def main() -> int:
                          "head-major with each token's K and V rows adjacent [Hkv][tok][2][d]")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-streamed", action="store_true")
-    ap.add_argument("--cpu-sample-requests", type=int, default=6)
+    ap.add_argument("--cpu-sample-requests", type=int, default=16,
+                    help="requests of the workload the fp64 oracle is timed on (16 = all of config 3, ~10 s)")
     ap.add_argument("--per-launch-only", action="store_true",
                     help="only time the history-chunk launches (for profiler runs)")
     ap.add_argument("--copy-probe", action="store_true",
