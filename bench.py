@@ -432,6 +432,8 @@ def main() -> int:
                          "head-major with each token's K and V rows adjacent [Hkv][tok][2][d]")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-streamed", action="store_true")
+    ap.add_argument("--streamed-only", action="store_true",
+                    help="only the streamed round (for memory-copy profiles of the host link)")
     ap.add_argument("--cpu-sample-requests", type=int, default=16,
                     help="requests of the workload the fp64 oracle is timed on (16 = all of config 3, ~10 s)")
     ap.add_argument("--per-launch-only", action="store_true",
@@ -482,6 +484,15 @@ def main() -> int:
     torch.cuda.synchronize()
 
     batch = w.num_chunks if args.batch == 0 else args.batch
+    if args.streamed_only:
+        t_stream, t_h2d, h2d_bytes, same = streamed_round(torch, H, w, b, chunks, stream, max(1, args.steps))
+        print(json.dumps({"streamed_only": {"workload": w.name, "rounds": max(1, args.steps),
+                                            "round_ms": round(t_stream * 1e3, 3), "h2d_only_ms": round(t_h2d * 1e3, 3),
+                                            "host_link_GBs": round(h2d_bytes / t_h2d / 1e9, 2),
+                                            "bitwise_equal_to_in_hbm": same}}), flush=True)
+        del b, chunks
+        torch.cuda.synchronize()
+        return 0
     if args.per_launch_only:
         times = per_launch_times(torch, ss, b, chunks, stream, max(1, args.steps), batch)
         mean = sum(t for t, _ in times) / len(times)
