@@ -430,6 +430,9 @@ def main() -> int:
     ap.add_argument("--kv-layout", choices=["token", "head", "head-kv"], default="head",
                     help="history chunk layout: token-major [tok][Hkv][d], head-major [Hkv][tok][d] or "
                          "head-major with each token's K and V rows adjacent [Hkv][tok][2][d]")
+    ap.add_argument("--balance-permille", type=int, default=0,
+                    help="ss_round_desc.balance_permille: share of each workgroup's tokens left to the "
+                         "cross-die balancing tail (0 = the library's default, -1 = no tail)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-streamed", action="store_true")
     ap.add_argument("--streamed-only", action="store_true",
@@ -478,7 +481,8 @@ def main() -> int:
                      head_dim=w.head_dim, chunk_tokens=w.chunk_tokens, cfg_id=args.config)
     log(f"bench: config {args.config} ({w.name}): generating inputs on the GPU")
     layout = {"token": ss.SS_KV_TOKEN_MAJOR, "head": ss.SS_KV_HEAD_MAJOR, "head-kv": ss.SS_KV_HEAD_MAJOR_KV}[args.kv_layout]
-    b = H.RoundBuffers(w, split_tokens=args.split_tokens, kv_layout=layout, mfma_min_rows=args.mfma_min_rows)
+    b = H.RoundBuffers(w, split_tokens=args.split_tokens, kv_layout=layout, mfma_min_rows=args.mfma_min_rows,
+                       balance_permille=args.balance_permille)
     chunks = H.hbm_history(w, kv_layout=layout)
     stream = torch.cuda.Stream()
     torch.cuda.synchronize()

@@ -94,6 +94,14 @@ typedef struct {
                                [Hkv][sum_b len_b][d] or SS_KV_HEAD_MAJOR_KV
                                [Hkv][sum_b len_b][2][d] (K and V rows of a
                                token adjacent)                                 */
+  int32_t balance_permille; /* thousandths of every workgroup share held back
+                               as a tail of small units that workgroups of
+                               any KV head claim once their own share is done
+                               (the GPU's dies stream at different rates);
+                               0 = default (100), < 0 = no tail, at most 500.
+                               Applies to history calls whose shares hold at
+                               least 4096 tokens; the result is the same
+                               bitwise whichever workgroup attends a unit      */
 } ss_round_desc;
 
 /* History chunk layouts (ss_round_desc.kv_layout).  In all, request b's
@@ -107,8 +115,9 @@ typedef struct {
 #define SS_KV_HEAD_MAJOR_KV 2
 
 /* Bytes of device workspace a round with this descriptor needs (fp32
- * online-softmax states of every query row, per split slot).  0 if the
- * descriptor is invalid (see ss_last_error). */
+ * online-softmax states of every query row, per split slot, and 256 bytes of
+ * claim counters for the balanced history calls).  0 if the descriptor is
+ * invalid (see ss_last_error). */
 size_t ss_round_workspace_bytes(const ss_round_desc *desc);
 
 /* Start a round (paper Sec. 4.2: state (m, l, a) = (-inf, 0, 0) per query and
@@ -117,7 +126,9 @@ size_t ss_round_workspace_bytes(const ss_round_desc *desc);
  * workspace: device, 256-byte aligned, >= ss_round_workspace_bytes(desc);
  * owned by the round until finalize's work has completed.  The empty state
  * is tracked on the host (a split slot is written before it is ever read),
- * so this call currently enqueues nothing on `stream`.
+ * so this call enqueues nothing on `stream`; the round's first history call
+ * with a balancing tail enqueues a one-wave kernel that zeroes the claim
+ * counters before its attention launch.
  * On success *out receives a new handle (free with ss_round_destroy). */
 ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q,
                         void *workspace, size_t workspace_bytes, hipStream_t stream);

@@ -18,6 +18,7 @@ constexpr int kWaves = 4;           // waves per workgroup of the chunk kernels
 constexpr int kMaxCand = 8;         // candidates per request (k_b + 1)
 constexpr int kMaxValuRows = 4;     // rows per KV head the VALU chunk kernel handles
 constexpr int kMaxRows = 32;        // rows per KV head the MFMA chunk kernel handles
+constexpr int kClaimCounters = 64;  // balanced history launches per round (one claim counter each)
 
 // Unit kinds: the chunk kernel body that attends a unit (rows per KV head
 // M = n_b * G: <= 4 on the VALU path, else MFMA with ceil(M / 16) blocks).
@@ -78,6 +79,13 @@ struct ChunkHeader {
   uint64_t head_stride[kMaxChunks];   // elements between KV heads at the same token
   int32_t num_units;
   int32_t num_wgs;      // workgroups per KV head (grid.y)
+  // Balancing tail: units [tail_first, tail_first + num_tail) are claimed at
+  // run time, for every KV head, by whichever workgroup has finished its own
+  // units: claim c = atomicAdd(claim, 1) < num_tail * Hkv attends unit
+  // tail_first + c / Hkv for KV head c % Hkv.  The counter is zero at launch.
+  uint32_t *claim;
+  int32_t tail_first;
+  int32_t num_tail;
 };
 
 template <int MaxUnits, int MaxItems, int MaxWgs>
@@ -118,5 +126,8 @@ using FinalParams = FinalParamsT<kMaxItems>;
 hipError_t launch_chunk(const ChunkParams &p, hipStream_t s);
 // Speculative Frontier pass fused with the split-slot merge and O = a / l.
 hipError_t launch_finalize(const FinalParams &p, hipStream_t s);
+// Zero n claim counters (a kernel rather than a memset node, so the call
+// can be captured in a graph).
+hipError_t launch_clear_claims(uint32_t *counters, int n, hipStream_t s);
 
 }  // namespace ss

@@ -250,13 +250,12 @@ __device__ __forceinline__ s16x4_t lds_read_tr16(const unsigned char *p) {
 }
 
 template <int RB, typename P>
-__device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i0, int nit, int tx) {
+__device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i0, int nit, int tx, int g) {
   const int w = __builtin_amdgcn_readfirstlane(tx >> 6);   // wave-uniform
   const int lane = tx & 63;
   const int lr = lane & 15;
   const int lq = lane >> 4;
   const Item it = p.items[i0];          // request, slot and flags of the whole chain
-  const int g = blockIdx.x;
   const int M = it.n_cand * p.G;
   int ntiles = 0;
   for (int k = 0; k < nit; ++k) ntiles += tiles_of(p.items[i0 + k]);
@@ -480,13 +479,12 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i
 // reduced over the 16 lanes of a DPP row.
 // ---------------------------------------------------------------------------
 template <int MAXR, typename P>
-__device__ __forceinline__ void valu_unit(const P &p, float *smem, int i0, int nit, int tx) {
+__device__ __forceinline__ void valu_unit(const P &p, float *smem, int i0, int nit, int tx, int g) {
   const int w = __builtin_amdgcn_readfirstlane(tx >> 6);   // wave-uniform
   const int lane = tx & 63;
   const int c = lane & 15;
   const int tg = lane >> 4;
   const Item it = p.items[i0];          // request, slot and flags of the whole chain
-  const int g = blockIdx.x;
   const int M = it.n_cand * p.G;
   int ntiles = 0;
   for (int k = 0; k < nit; ++k) ntiles += tiles_of(p.items[i0 + k]);
@@ -654,38 +652,70 @@ static_assert(MfmaLds<1>::kBytes <= kChunkLdsBytes, "LDS sizes");
 
 // ---------------------------------------------------------------------------
 // History kernel: one launch for every unit of a call.  Workgroup =
-// (kv head, w) = (blockIdx.x, blockIdx.y) attends the units of its list in
-// order (the host gives every workgroup an equal share of the call's
-// tokens, which may span several requests); each unit's kind selects the
-// body: MFMA with two or one 16-row blocks, or the VALU path for <= 4 rows
-// (when the round asks for it).  The heads are the fast grid dimension: with
-// 8 KV heads the round-robin placement gives every XCD one head of every
-// workgroup's share.
+// (kv head, w) = (blockIdx.x, blockIdx.y) first attends the units of its own
+// list in order (the host gives every workgroup an equal share of the
+// call's tokens, which may span several requests); each unit's kind selects
+// the body: MFMA with two or one 16-row blocks, or the VALU path for <= 4
+// rows (when the round asks for it).  The heads are the fast grid dimension:
+// with 8 KV heads the round-robin placement gives every XCD one head of
+// every workgroup's share.
+//
+// The XCDs do not stream at the same rate (on MI355X some finish an equal
+// share 10% later than others), so the host may hold back the last part of
+// every share as a tail of small units, largest first.  A workgroup that has
+// finished its own list claims (tail unit, KV head) pairs from a counter
+// until none is left, whatever its own head; each tail unit still owns a
+// fixed state slot, so the result does not depend on who attends it.
 // ---------------------------------------------------------------------------
 template <typename P>
 __global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[kChunkLdsBytes];
+  __shared__ int claim_sh;
   const int u0 = p.wg_first[blockIdx.y];
   const int u1 = p.wg_first[blockIdx.y + 1];
-  for (int u = u0; u < u1; ++u) {
-    if (u != u0) __syncthreads();   // the previous unit's fold has read the LDS this unit restages
+  const int nclaims = p.num_tail * p.Hkv;
+  int u = u0;
+  bool first = true;
+  for (;;) {
+    int uidx, g;
+    if (u < u1) {
+      if (!first) __syncthreads();   // the previous unit's fold has read the LDS this unit restages
+      uidx = u++;
+      g = blockIdx.x;
+    } else {
+      if (nclaims == 0) break;
+      if (!first) __syncthreads();   // ... and every thread has read the previous claim
+      if (threadIdx.x == 0) claim_sh = (int)atomicAdd(p.claim, 1u);
+      __syncthreads();
+      const int c = __builtin_amdgcn_readfirstlane(claim_sh);
+      if (c >= nclaims) break;
+      const int t = c / p.Hkv;
+      uidx = p.tail_first + t;
+      g = c - t * p.Hkv;
+    }
+    first = false;
     // The bodies derive their per-lane addresses from tx.  Passing it
     // through an empty asm each unit keeps the compiler from computing
     // them once before the loop and holding all three bodies' worth live
     // across it (that spilled 14 registers and cost 6% on one-unit calls).
     int tx = threadIdx.x;
     asm volatile("" : "+v"(tx));
-    const uint32_t unit = p.units[u];
+    const uint32_t unit = p.units[uidx];
     const int i0 = unit & 0xffff;
     const int nit = (unit >> 16) & 0xff;
     const int kind = unit >> 24;
     if (kind == kUnitMfma2)
-      mfma_unit<2>(p, smem, i0, nit, tx);
+      mfma_unit<2>(p, smem, i0, nit, tx, g);
     else if (kind == kUnitMfma1)
-      mfma_unit<1>(p, smem, i0, nit, tx);
+      mfma_unit<1>(p, smem, i0, nit, tx, g);
     else
-      valu_unit<kMaxValuRows>(p, reinterpret_cast<float *>(smem), i0, nit, tx);
+      valu_unit<kMaxValuRows>(p, reinterpret_cast<float *>(smem), i0, nit, tx, g);
   }
+}
+
+__global__ void clear_claims_kernel(uint32_t *c, int n) {
+  const int i = threadIdx.x;
+  if (i < n) c[i] = 0u;
 }
 
 // ---------------------------------------------------------------------------
@@ -831,6 +861,10 @@ hipError_t launch_chunk(const ChunkParams &p, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t launch_clear_claims(uint32_t *counters, int n, hipStream_t s) {
+  hipLaunchKernelGGL(clear_claims_kernel, dim3(1), dim3(kClaimCounters), 0, s, counters, n);
+  return hipGetLastError();
+}
 hipError_t launch_finalize(const FinalParams &p, hipStream_t s) {
   int rows = 0;
   for (int i = 0; i < p.num_items; ++i) rows = rows > p.items[i].n_cand * p.Hq ? rows : p.items[i].n_cand * p.Hq;

@@ -20,7 +20,7 @@ class RoundBuffers:
 
     def __init__(self, w: Workload, layer: int = 0, device="cuda", split_tokens: int = 0,
                  mfma_min_rows: int = 0, max_chunk_tokens: Optional[int] = None,
-                 kv_layout: int = ss.SS_KV_TOKEN_MAJOR):
+                 kv_layout: int = ss.SS_KV_TOKEN_MAJOR, balance_permille: int = 0):
         self.w = w
         self.layer = layer
         self.device = device
@@ -30,7 +30,7 @@ class RoundBuffers:
         mct = max_chunk_tokens or max(1, max(sum(w.chunk_lens(j)) for j in range(max(1, w.num_chunks))))
         self.kv_layout = kv_layout
         self.desc = ss.make_desc(w.num_cand, w.num_q_heads, w.num_kv_heads, w.head_dim, w.softmax_scale,
-                                 mct, split_tokens, mfma_min_rows, kv_layout)
+                                 mct, split_tokens, mfma_min_rows, kv_layout, balance_permille)
         self.ws_bytes = ss.ss_round_workspace_bytes(self.desc)
         if self.ws_bytes == 0:
             raise ss.SpecStreamError(ss.SS_ERR_INVALID_ARGUMENT, "ss_round_workspace_bytes", ss.ss_last_error())

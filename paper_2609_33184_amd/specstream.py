@@ -58,19 +58,20 @@ class ss_round_desc(ctypes.Structure):
         ("split_tokens", ctypes.c_int32),
         ("mfma_min_rows", ctypes.c_int32),
         ("kv_layout", ctypes.c_int32),
+        ("balance_permille", ctypes.c_int32),
     ]
 
 
 def make_desc(num_cand: Sequence[int], num_q_heads: int, num_kv_heads: int, head_dim: int = 128,
               softmax_scale: Optional[float] = None, max_chunk_tokens: int = 1 << 30,
-              split_tokens: int = 0, mfma_min_rows: int = 0, kv_layout: int = SS_KV_TOKEN_MAJOR
-              ) -> ss_round_desc:
+              split_tokens: int = 0, mfma_min_rows: int = 0, kv_layout: int = SS_KV_TOKEN_MAJOR,
+              balance_permille: int = 0) -> ss_round_desc:
     """Build a descriptor; the candidate-count array is kept alive on it."""
     arr = (ctypes.c_int32 * len(num_cand))(*[int(x) for x in num_cand])
     d = ss_round_desc(len(num_cand), num_q_heads, num_kv_heads, head_dim,
                       (head_dim ** -0.5) if softmax_scale is None else softmax_scale,
                       ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)), max_chunk_tokens, split_tokens,
-                      mfma_min_rows, kv_layout)
+                      mfma_min_rows, kv_layout, balance_permille)
     d._keep = arr
     return d
 

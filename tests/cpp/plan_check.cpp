@@ -9,6 +9,7 @@
 #include "specstream.h"
 #include <cstdio>
 #include <cstdlib>
+#include <cmath>
 #include <cstring>
 #include <map>
 #include <random>
@@ -16,9 +17,14 @@
 #include <set>
 
 namespace {
-struct Rec { std::vector<ss::Item> items; std::vector<uint32_t> units; std::vector<uint16_t> wg_first; int kind; };
+struct Rec {
+  std::vector<ss::Item> items; std::vector<uint32_t> units; std::vector<uint16_t> wg_first; int kind;
+  int tail_first, num_tail; uint32_t *claim; int clears_before;
+};
 std::vector<Rec> g_recs;
 const ss::ChunkParams *g_last = nullptr;
+int g_clears = 0;                 // claim-counter clear launches so far
+uint32_t *g_clear_ptr = nullptr;
 }
 
 namespace ss {
@@ -29,13 +35,22 @@ static void rec(const ChunkParams &p, int kind) {
   r.wg_first.assign(p.wg_first, p.wg_first + p.num_wgs + 1);
   if (p.num_wgs < 1 || p.num_wgs > kMaxWgs) { printf("bad workgroup count\n"); exit(1); }
   r.kind = kind;
+  r.tail_first = p.tail_first; r.num_tail = p.num_tail; r.claim = p.claim; r.clears_before = g_clears;
   if (p.num_units < 1 || p.num_units > kMaxUnits || p.num_items < 1 || p.num_items > kMaxItems) { printf("bad counts\n"); exit(1); }
   g_recs.push_back(r);
   g_last = &p;
 }
 hipError_t launch_chunk(const ChunkParams &p, hipStream_t) { rec(p, -1); return hipSuccess; }
 hipError_t launch_finalize(const FinalParams &, hipStream_t) { return hipSuccess; }
+hipError_t launch_clear_claims(uint32_t *c, int n, hipStream_t) {
+  if (n != kClaimCounters) { printf("clear of %d counters\n", n); exit(1); }
+  ++g_clears; g_clear_ptr = c; return hipSuccess;
 }
+}
+
+static const ss_round_desc *g_desc = nullptr;
+static std::set<uint32_t *> g_claim_used;
+static int g_tail_calls = 0;
 
 static int tiles_of(const ss::Item &it) { return (it.tok_count + ss::kTile - 1) / ss::kTile; }
 
@@ -70,7 +85,7 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
   long total = 0, wgs = 0, max_share = 0;
   for (auto &row : lens) for (int x : row) total += x;
   for (auto &rc : g_recs) {
-    CHECK(rc.wg_first.front() == 0 && rc.wg_first.back() == rc.units.size(), "workgroup table ends");
+    CHECK(rc.wg_first.front() == 0 && rc.wg_first.back() + rc.num_tail == rc.units.size(), "workgroup table ends");
     for (size_t w = 0; w + 1 < rc.wg_first.size(); ++w) {
       CHECK(rc.wg_first[w] <= rc.wg_first[w + 1], "workgroup table order");
       long share = 0;
@@ -83,6 +98,20 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
     }
   }
   if (total >= 32 * wgs) CHECK(max_share <= (total + wgs - 1) / wgs + 31, "share %ld > mean %ld + a tile", max_share, total / wgs);
+  // balancing tail: after the workgroups' own units, one launch per call,
+  // a counter of the workspace's own per balanced launch, zeroed once per round
+  for (auto &rc : g_recs) {
+    if (rc.num_tail == 0) { CHECK(rc.wg_first.back() == rc.units.size(), "units beyond the workgroup lists"); continue; }
+    CHECK(g_recs.size() == 1, "a call with a tail took %zu launches", g_recs.size());
+    CHECK(rc.tail_first == (int)rc.wg_first.back() && rc.tail_first + rc.num_tail == (int)rc.units.size(), "tail range");
+    CHECK(rc.clears_before == 1 && g_clear_ptr != nullptr, "claim counters cleared %d times before the launch", rc.clears_before);
+    const long idx = rc.claim - g_clear_ptr;
+    CHECK(idx >= 0 && idx < ss::kClaimCounters, "claim counter outside the cleared block");
+    CHECK((uintptr_t)g_clear_ptr == 0x7f1000000000ull + ss_round_workspace_bytes(g_desc) - 256, "claim block at the workspace end");
+    CHECK(!g_claim_used.count(rc.claim), "claim counter reused in one round");
+    g_claim_used.insert(rc.claim);
+    g_tail_calls++;
+  }
   for (auto &rc : g_recs) {
     for (size_t u = 0; u < rc.units.size(); ++u) {
       const int i0 = rc.units[u] & 0xffff, nit = (rc.units[u] >> 16) & 0xff, kind = rc.units[u] >> 24;
@@ -156,7 +185,7 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
 }
 
 static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> ncand, std::vector<int> hist, int S,
-                     int split, int layout, int batch, int mfma_min_rows = 0) {
+                     int split, int layout, int batch, int mfma_min_rows = 0, int balance = 0, int expect_tail = -1) {
   const int nch = [&] { int m = 0; for (int h : hist) m = std::max(m, (h + S - 1) / S); return m; }();
   std::vector<std::vector<int>> lens(nch, std::vector<int>(B));
   long maxc = 1;
@@ -164,6 +193,8 @@ static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> 
   ss_round_desc d{};
   d.num_requests = B; d.num_q_heads = Hq; d.num_kv_heads = Hkv; d.head_dim = 128; d.softmax_scale = 0.088f;
   d.num_cand = ncand.data(); d.max_chunk_tokens = (int)maxc; d.split_tokens = split; d.mfma_min_rows = mfma_min_rows; d.kv_layout = layout;
+  d.balance_permille = balance;
+  g_desc = &d; g_clears = 0; g_clear_ptr = nullptr; g_claim_used.clear(); g_tail_calls = 0;
   ss_round *r = nullptr;
   size_t ws = ss_round_workspace_bytes(&d);
   ss_status s = ss_round_init(&r, &d, (const void *)0x7f0000000000ull, (void *)0x7f1000000000ull, ws, nullptr);
@@ -179,7 +210,10 @@ static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> 
     check_call(B, Hq, Hkv, ncand, part, split, layout, mfma_min_rows, used, r);
   }
   ss_round_destroy(r);
-  printf("%-44s %s (launches in last call: %zu)\n", name, fails == before ? "ok" : "FAILED", g_recs.size());
+  CHECK(g_clears == (g_tail_calls > 0 ? 1 : 0), "%d clears for %d balanced calls", g_clears, g_tail_calls);
+  if (expect_tail >= 0) CHECK((g_tail_calls > 0) == (expect_tail > 0), "%s: %d balanced calls", name, g_tail_calls);
+  printf("%-44s %s (launches in last call: %zu, balanced calls: %d)\n", name, fails == before ? "ok" : "FAILED",
+         g_recs.size(), g_tail_calls);
 }
 
 int main() {
@@ -190,11 +224,25 @@ int main() {
     scenario("config1 split 96", 1, 8, 2, {5}, {4096}, 1024, 96, layout, 1);
     scenario("config1 batched", 1, 8, 2, {5}, {4096}, 1024, 0, layout, 4);
     scenario("config2 per-chunk", 1, 32, 8, {5}, {16384}, 2048, 0, layout, 1);
-    scenario("config3 batched 8", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8);
+    scenario("config3 batched 8", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 1);
+    scenario("config3 batched 8, no tail", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, -1, 0);
+    scenario("config3 batched 8, tail 500", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 500, 1);
+    scenario("config3 batched 8, tail 1", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 1, 1);
     scenario("config3 per-chunk", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 1);
     scenario("config3 batched 3", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 3);
     scenario("config3 split 2048 batched", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 2048, layout, 8);
-    scenario("config5 per-chunk", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 1);
+    scenario("config5 per-chunk", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 1, 0, 0, 1);
+    {
+      std::mt19937 g4(4);
+      std::vector<int> h4(64), n4(64);
+      for (int b = 0; b < 64; ++b) {
+        h4[b] = (int)std::lround(std::exp(std::log(2048.0) + (std::log(65536.0) - std::log(2048.0)) * (g4() / 4294967296.0)));
+        n4[b] = 1 + g4() % 8;
+      }
+      scenario("config4-like ragged batched 16", 64, 32, 8, n4, h4, 4096, 0, layout, 16, 0, 0, 1);
+      scenario("config4-like ragged per-chunk", 64, 32, 8, n4, h4, 4096, 0, layout, 1, 0, 0, -1);
+    }
+    scenario("config2 per-chunk (no tail: small shares)", 1, 32, 8, {5}, {16384}, 2048, 0, layout, 8, 0, 0, 0);
     scenario("config5 batched 16", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 16);
     scenario("many units (8192 chains)", 256, 8, 2, std::vector<int>(256, 3), std::vector<int>(256, 4096), 512, 128, layout, 8);
     scenario("many items (chains of 16)", 128, 8, 2, std::vector<int>(128, 2), std::vector<int>(128, 8192), 32, 512, layout, 32);
@@ -209,7 +257,8 @@ int main() {
       const int batch = 1 + rng() % 32;
       const int hq = (rng() % 2) ? 32 : 8, hkv = hq == 32 ? 8 : 2;
       char nm[64]; snprintf(nm, sizeof nm, "random %d B=%d S=%d split=%d batch=%d", rep, B, S, split, batch);
-      scenario(nm, B, hq, hkv, nc, h, S, split, layout, batch, (int)(rng() % 6));
+      const int bal = (rng() % 4 == 0) ? -1 : (rng() % 2 ? 0 : (int)(1 + rng() % 500));
+      scenario(nm, B, hq, hkv, nc, h, S, split, layout, batch, (int)(rng() % 6), bal);
     }
   }
   printf("%s\n", fails ? "FAILURES" : "all ok");

@@ -62,7 +62,7 @@ def _ws(cands, hq):
     rows = sum(cands) * hq
     a = -(-32 * rows * 128 * 4 // 256) * 256
     m = -(-32 * rows * 4 // 256) * 256
-    return a + 2 * m
+    return a + 2 * m + 256          # + the claim counters of the balanced history calls
 
 
 def test_workspace_bytes_and_descriptor_validation(lib):
@@ -82,6 +82,7 @@ def test_workspace_bytes_and_descriptor_validation(lib):
         (ss.make_desc([4], 8, 2, mfma_min_rows=6), "mfma_min_rows"),
         (ss.make_desc([4], 8, 2, kv_layout=3), "kv_layout"),
         (ss.make_desc([4], 8, 2, max_chunk_tokens=0), "max_chunk_tokens"),
+        (ss.make_desc([4], 8, 2, balance_permille=501), "balance_permille"),
     ]
     for desc, word in bad:
         assert ss.ss_round_workspace_bytes(desc) == 0

@@ -34,7 +34,7 @@ LAYOUT_IDS = ["token_major", "head_major", "head_major_kv"]
 
 def _run(w, stream, kv_layout=ss.SS_KV_TOKEN_MAJOR, **kw):
     b = H.RoundBuffers(w, split_tokens=kw.pop("split_tokens", 0), mfma_min_rows=kw.pop("mfma_min_rows", 0),
-                       kv_layout=kv_layout)
+                       kv_layout=kv_layout, balance_permille=kw.pop("balance_permille", 0))
     chunks = H.hbm_history(w, kv_layout=kv_layout)
     torch.cuda.synchronize()
     H.run_round(b, chunks, stream.cuda_stream, **kw)
@@ -188,3 +188,32 @@ def test_repeat_is_bitwise_deterministic(stream):
         b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR, batch=w.num_chunks)
         outs.append((b.out.clone(), b.lse.clone()))
     assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+
+
+def test_balancing_tail_independent_of_claim_order(stream):
+    """Cross-die balancing: the tail units of a launch go to whichever
+    workgroups claim them first, so who attends what differs between
+    launches.  Each unit still owns one state slot, so repeats are bitwise
+    equal; the static split (no tail) and the largest tail give the same
+    result up to the rounding of a different slot partition, and both match
+    the oracle.  Config 4 in one batched call, then config 3 as three calls
+    (the later calls' tail units merge into slots the first call wrote)."""
+    w = W.workload(4)
+    runs = {}
+    for bal in (0, 0, -1, 500):
+        print(f"config 4 batched, balance_permille {bal}", flush=True)
+        b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR, batch=w.num_chunks, balance_permille=bal)
+        runs.setdefault(bal, []).append((b.out.clone(), b.lse.clone()))
+        if bal == 500:
+            check_sampled(w, b.out, b.lse, [(2, 7), (40, 0)], what="config4 tail 500")
+    (o0, l0), (o1, l1) = runs[0]
+    assert torch.equal(o0, o1) and torch.equal(l0, l1)
+    for bal in (-1, 500):
+        o, _ = runs[bal][0]
+        rel = float(torch.linalg.norm((o - o0).double()) / torch.linalg.norm(o0.double()))
+        print(f"balance {bal} vs default: rel-L2 {rel:.3e}", flush=True)
+        assert rel <= 1e-5
+    w = W.workload(3)
+    print("config 3, three history calls (3 + 3 + 2 chunks), tail 250", flush=True)
+    b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR, batch=3, balance_permille=250)
+    check_sampled(w, b.out, b.lse, [(0, 0), (9, 7), (15, 3)], what="config3 3 calls tail 250")
