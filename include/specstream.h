@@ -99,9 +99,10 @@ typedef struct {
                                any KV head claim once their own share is done
                                (the GPU's dies stream at different rates);
                                0 = default (100), < 0 = no tail, at most 500.
-                               Applies to history calls whose shares hold at
-                               least 4096 tokens; the result is the same
-                               bitwise whichever workgroup attends a unit      */
+                               The default applies to history calls whose
+                               shares hold at least 24576 tokens, a value set
+                               here from 4096; the result is the same bitwise
+                               whichever workgroup attends a unit              */
 } ss_round_desc;
 
 /* History chunk layouts (ss_round_desc.kv_layout).  In all, request b's

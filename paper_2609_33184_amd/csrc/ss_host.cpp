@@ -62,18 +62,21 @@ constexpr int kMinPiece = 256;   // tokens per workgroup at least
 // thousandths of every share become tail units of guided sizes, each about
 // 2 (tail tokens left) / W tokens, clamped to [kTailMin, kTailMax] and to
 // the share's own tail, so the first claims are large and the last ones
-// small.  Only calls whose shares have at least kTailMinShare tokens get a
-// tail.  Measured on MI355X (means of two runs, one batched call): 64
-// ragged requests 667 -> 642 us, 32 x 131072 tokens 2505 -> 2423 us, 16 x
-// 32768 tokens 321 -> 320 us; a tail of 150 thousandths, or pieces a
-// quarter of that size, gained less (per-workgroup timestamps: a claimed
-// unit costs a few microseconds of start-up and merge, and the 16 x 32768
+// small.  Only calls whose shares have at least kTailMinShare tokens get
+// the default tail (kTailMinShareExplicit for a fraction the caller set).  Measured on MI355X (means of two runs, one batched call): 64
+// ragged requests (shares of ~32K tokens) 667 -> 642 us, 32 x 131072
+// tokens (shares of 131072) 2505 -> 2423 us; a tail of 150 thousandths, or
+// pieces a quarter of that size, gained less.  Per-workgroup timestamps of
+// 16 x 32768 tokens (shares of 16384) show the launch 3 us shorter, less
+// than the claim-counter clear launch the round then needs (4.4 us): a
+// claimed unit costs about 4 us of start-up, claim and merge, and that
 // launch is already at the HBM throughput of the longer ones minus its
-// fixed start and end costs).
+// fixed start and end costs.
 constexpr int kDefaultTailPermille = 100;
 constexpr long kTailMin = 256;
 constexpr long kTailMax = 4096;
-constexpr long kTailMinShare = 4096;
+constexpr long kTailMinShare = 24576;          // with the default tail
+constexpr long kTailMinShareExplicit = 4096;   // with a tail the caller asked for
 // Body for few rows per KV head: the MFMA body with padded rows by default.
 // With non-temporal K/V loads the fp32 VALU body became compute-bound (VALU
 // 72% busy): 16 x 32768 tokens with 4 rows per KV head took 396-399 us on
@@ -397,7 +400,8 @@ ss_status plan_chunks(const ss_round *r, int nchunks, const int32_t *len, const 
   // counter is left; coarser pieces if the finer ones need too many slots
   // or table entries, else none.
   const int permille = r->tail_permille == 0 ? kDefaultTailPermille : r->tail_permille;
-  if (permille > 0 && total / W >= kTailMinShare && r->balanced_launches < ss::kClaimCounters &&
+  const long min_share = r->tail_permille == 0 ? kTailMinShare : kTailMinShareExplicit;
+  if (permille > 0 && total / W >= min_share && r->balanced_launches < ss::kClaimCounters &&
       fits_one_launch(*plan)) {
     Plan t;
     for (long tmin = kTailMin; tmin <= kTailMax; tmin *= 2)

@@ -224,14 +224,16 @@ int main() {
     scenario("config1 split 96", 1, 8, 2, {5}, {4096}, 1024, 96, layout, 1);
     scenario("config1 batched", 1, 8, 2, {5}, {4096}, 1024, 0, layout, 4);
     scenario("config2 per-chunk", 1, 32, 8, {5}, {16384}, 2048, 0, layout, 1);
-    scenario("config3 batched 8", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 1);
+    scenario("config3 batched 8", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 0);
+    scenario("16 x 65536 batched 16 (tail)", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 65536), 4096, 0, layout, 16, 0, 0, 1);
     scenario("config3 batched 8, no tail", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, -1, 0);
     scenario("config3 batched 8, tail 500", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 500, 1);
     scenario("config3 batched 8, tail 1", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 1, 1);
     scenario("config3 per-chunk", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 1);
     scenario("config3 batched 3", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 3);
     scenario("config3 split 2048 batched", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 2048, layout, 8);
-    scenario("config5 per-chunk", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 1, 0, 0, 1);
+    scenario("config5 per-chunk", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 1, 0, 0, 0);
+    scenario("config5 batched 4 (tail)", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 4, 0, 0, 1);
     {
       std::mt19937 g4(4);
       std::vector<int> h4(64), n4(64);
