@@ -232,6 +232,29 @@ def round_times(torch, H, b, chunks, stream, rounds: int, batch: int, flush=None
     return sorted(e0.elapsed_time(e1) / 1e3 for e0, e1 in evs)
 
 
+def back_to_back(torch, H, b, chunks, stream, rounds: int, batch: int):
+    """Mean time per round of `rounds` rounds enqueued back to back: eager
+    calls, and replays of the round captured in a HIP graph."""
+    def timed(step):
+        for _ in range(5):
+            step()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(rounds):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / rounds
+    eager = timed(lambda: H.run_round(b, chunks, stream.cuda_stream, batch=batch))
+    g = H.capture_round(b, chunks, batch=batch)
+    with torch.cuda.stream(stream):
+        graph = timed(g.replay)
+    del g
+    return {"eager_calls": round(eager, 2), "graph_replay": round(graph, 2)}
+
+
 def pct(xs, q):
     i = min(len(xs) - 1, max(0, int(round(q * (len(xs) - 1)))))
     return xs[i]
@@ -260,6 +283,10 @@ def config_table(torch, H, ss, W, stream, layout: int, rounds: int):
                            "effective_KV_GBs_p50": round(kv / p50 / 1e9, 2),
                            "pct_of_hbm_peak_p50": round(100.0 * kv / p50 / 1e9 / HBM_PEAK_GBS, 2),
                            "cache_flushed_between_rounds": flush is not None}
+        if flush is not None:
+            # the same round back to back (its history then stays in the last-level cache): the eager
+            # calls, where the host's per-call work sets the pace, against replays of a captured graph
+            table[str(cfg)]["back_to_back_cache_resident_us"] = back_to_back(torch, H, b, chunks, stream, rounds, batch)
         del b, chunks, flush
         torch.cuda.synchronize()
         torch.cuda.empty_cache()

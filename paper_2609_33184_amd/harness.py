@@ -91,6 +91,23 @@ def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor
         ss.ss_round_destroy(r)
 
 
+def capture_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor]], batch: int = 1,
+                  pool=None) -> "torch.cuda.CUDAGraph":
+    """Capture one whole round (the same calls as run_round) into a HIP graph.
+
+    Every step the library enqueues is a kernel launch with its arguments by
+    value (no memsets, no host waits), so a replay redoes the round on the
+    buffers it was captured with: b.q, b.kc, b.vc, the chunks, b.ws and
+    b.out / b.lse.  Replays serve loops that re-run a round of the same
+    shape with new contents in those buffers, without the host's per-call
+    work."""
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, pool=pool):
+        run_round(b, chunks, torch.cuda.current_stream().cuda_stream, batch=batch)
+    return g
+
+
 class HostHistory:
     """One layer's history in pinned host memory, chunk j as its K then its V
     (each in the round's chunk layout; with the interleaved layout the chunk's

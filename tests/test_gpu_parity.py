@@ -217,3 +217,32 @@ def test_balancing_tail_independent_of_claim_order(stream):
     print("config 3, three history calls (3 + 3 + 2 chunks), tail 250", flush=True)
     b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR, batch=3, balance_permille=250)
     check_sampled(w, b.out, b.lse, [(0, 0), (9, 7), (15, 3)], what="config3 3 calls tail 250")
+
+
+def test_graph_replay_matches_eager(stream):
+    """A round captured in a HIP graph (history launches, the claim-counter
+    clear of a balanced call, finalize) replays to bitwise the eager result,
+    replay after replay, with eager work and host synchronisations between
+    the replays (outputs overwritten, the workspace reused by an eager round
+    of another shape)."""
+    for cfg in (1, 4):
+        w = W.workload(cfg)
+        batch = w.num_chunks
+        print(f"config {cfg}: eager round, then graph capture and 3 replays", flush=True)
+        b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR, batch=batch)
+        ref_o, ref_l = b.out.clone(), b.lse.clone()
+        chunks = H.hbm_history(w, kv_layout=ss.SS_KV_HEAD_MAJOR)
+        g = H.capture_round(b, chunks, batch=batch)
+        for rep in range(3):
+            b.out.fill_(float("nan"))
+            b.lse.fill_(float("nan"))
+            b.ws.fill_(0xFF)                      # garbage state slots and claim counters
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(b.out, ref_o) and torch.equal(b.lse, ref_l), f"config {cfg} replay {rep}"
+            H.run_round(b, chunks, stream.cuda_stream, batch=1)   # eager per-chunk round on the same buffers
+            stream.synchronize()
+        del g
+        if cfg == 4:
+            check_sampled(w, b.out, b.lse, [(7, 2)], what="config4 after replays (eager per-chunk round)")
