@@ -83,7 +83,9 @@ typedef struct {
                                tokens (all requests, in request order) are
                                split into equal shares of about this many,
                                one per workgroup and KV head; 0 = automatic
-                               (one workgroup per CU); else a multiple of 32  */
+                               (one workgroup per CU, two per CU for calls
+                               whose shares would be below 2048 tokens);
+                               else a multiple of 32                           */
   int32_t mfma_min_rows;    /* rows per KV head (n_b * G) from which the bf16
                                MFMA path is used; fewer (at most 4) use the
                                fp32 VALU path.  0 = default (1: always MFMA,

@@ -57,7 +57,16 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // per-request pieces in longest-first order and 678-681 us with equal
 // shares (same GPU, same run).
 constexpr long kTargetWorkgroups = 256;
-constexpr int kMinPiece = 256;   // tokens per workgroup at least
+// Calls whose shares would be shorter than kSmallShare tokens at one
+// workgroup per CU are latency-bound: each wave walks its few tiles one
+// HBM round trip after another.  They get twice the workgroups (two fit on
+// a CU), with shares of at least kMinPiece tokens (one tile per wave), as
+// far as the state slots allow.  Measured on MI355X: 1 x 4096 tokens, 2 KV
+// heads, one batched call, 9.9 -> 7.5 us (64 workgroups instead of 32);
+// 1 x 16384 tokens, 8 KV heads (which would need 64 slots) took 16.5
+// against 17.0 us with 64 slots, which made finalize slower.
+constexpr long kSmallShare = 2048;
+constexpr int kMinPiece = 128;
 // Balancing tail (see the history kernel): the last kDefaultTailPermille
 // thousandths of every share become tail units of guided sizes, each about
 // 2 (tail tokens left) / W tokens, clamped to [kTailMin, kTailMax] and to
@@ -372,6 +381,7 @@ ss_status plan_chunks(const ss_round *r, int nchunks, const int32_t *len, const 
     W = (total + r->split_tokens - 1) / r->split_tokens;
   } else {
     W = std::max<long>(1, kTargetWorkgroups / r->Hkv);
+    if (total / W < kSmallShare) W = std::max<long>(1, 2 * kTargetWorkgroups / r->Hkv);
     W = std::min(W, std::max<long>(1, total / kMinPiece));
   }
   W = std::max<long>(1, std::min<long>(W, total));

@@ -60,7 +60,7 @@ def test_status_strings(lib):
 
 def _ws(cands, hq):
     rows = sum(cands) * hq
-    a = -(-32 * rows * 128 * 4 // 256) * 256
+    a = -(-32 * rows * 128 * 4 // 256) * 256     # 32 state slots per row
     m = -(-32 * rows * 4 // 256) * 256
     return a + 2 * m + 256          # + the claim counters of the balanced history calls
 
