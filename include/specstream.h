@@ -102,7 +102,7 @@ typedef struct {
                                (the GPU's dies stream at different rates);
                                0 = default (100), < 0 = no tail, at most 500.
                                The default applies to history calls whose
-                               shares hold at least 24576 tokens, a value set
+                               shares hold at least 16384 tokens, a value set
                                here from 4096; the result is the same bitwise
                                whichever workgroup attends a unit              */
 } ss_round_desc;

@@ -72,19 +72,20 @@ constexpr int kMinPiece = 128;
 // 2 (tail tokens left) / W tokens, clamped to [kTailMin, kTailMax] and to
 // the share's own tail, so the first claims are large and the last ones
 // small.  Only calls whose shares have at least kTailMinShare tokens get
-// the default tail (kTailMinShareExplicit for a fraction the caller set).  Measured on MI355X (means of two runs, one batched call): 64
-// ragged requests (shares of ~32K tokens) 667 -> 642 us, 32 x 131072
-// tokens (shares of 131072) 2505 -> 2423 us; a tail of 150 thousandths, or
-// pieces a quarter of that size, gained less.  Per-workgroup timestamps of
-// 16 x 32768 tokens (shares of 16384) show the launch 3 us shorter, less
-// than the claim-counter clear launch the round then needs (4.4 us): a
-// claimed unit costs about 4 us of start-up, claim and merge, and that
-// launch is already at the HBM throughput of the longer ones minus its
-// fixed start and end costs.
+// the default tail (kTailMinShareExplicit for a fraction the caller set).
+// Measured on MI355X, one batched call, tail on against off, alternated in
+// one session: 64 ragged requests (shares of ~32K tokens) 667 -> 642 us;
+// 32 x 131072 tokens (shares of 131072) 2505 -> 2423 us; 16 x 32768 tokens
+// (shares of 16384) 321.0 -> 319.6 us on a GPU whose XCDs finished their
+// shares within 278-309 us, and 344.2 -> 337.4 us on one where they
+// finished within 290-340 us.  A tail of 150 thousandths, or pieces a
+// quarter of that size, gained less.  A claimed unit costs about 4 us of
+// start-up, claim and merge, and a round's first balanced launch needs the
+// counter clear (about 4 us), so shorter shares are left alone.
 constexpr int kDefaultTailPermille = 100;
 constexpr long kTailMin = 256;
 constexpr long kTailMax = 4096;
-constexpr long kTailMinShare = 24576;          // with the default tail
+constexpr long kTailMinShare = 16384;          // with the default tail
 constexpr long kTailMinShareExplicit = 4096;   // with a tail the caller asked for
 // Body for few rows per KV head: the MFMA body with padded rows by default.
 // With non-temporal K/V loads the fp32 VALU body became compute-bound (VALU

@@ -733,7 +733,7 @@ __global__ void clear_claims_kernel(uint32_t *c, int n) {
 // independent chains; the frontier terms are summed first, then each group
 // of slots is folded in with the rescaled update of Eq. 14.
 // ---------------------------------------------------------------------------
-constexpr int kFinGroup = 32;
+constexpr int kFinGroup = 16;
 
 template <typename P>
 __global__ void __launch_bounds__(256) finalize_kernel(const P p) {

@@ -224,7 +224,8 @@ int main() {
     scenario("config1 split 96", 1, 8, 2, {5}, {4096}, 1024, 96, layout, 1);
     scenario("config1 batched", 1, 8, 2, {5}, {4096}, 1024, 0, layout, 4);
     scenario("config2 per-chunk", 1, 32, 8, {5}, {16384}, 2048, 0, layout, 1);
-    scenario("config3 batched 8", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 0);
+    scenario("config3 batched 8", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 1);
+    scenario("16 x 16384 batched 4 (no tail: shares of 8192)", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 16384), 4096, 0, layout, 4, 0, 0, 0);
     scenario("16 x 65536 batched 16 (tail)", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 65536), 4096, 0, layout, 16, 0, 0, 1);
     scenario("config3 batched 8, no tail", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, -1, 0);
     scenario("config3 batched 8, tail 500", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 500, 1);
