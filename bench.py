@@ -255,6 +255,13 @@ def back_to_back(torch, H, b, chunks, stream, rounds: int, batch: int):
     return {"eager_calls": round(eager, 2), "graph_replay": round(graph, 2)}
 
 
+def unit_blocks(w) -> str:
+    """The 16-row MFMA blocks of the workload's units (rows per KV head = candidates x GQA group)."""
+    blocks = sorted({-(-n * w.group // 16) for n in w.num_cand})
+    txt = "/".join(str(x) for x in blocks) + "-block"
+    return txt + (" (wide kernel)" if blocks[-1] > 2 else "")
+
+
 def pct(xs, q):
     i = min(len(xs) - 1, max(0, int(round(q * (len(xs) - 1)))))
     return xs[i]
@@ -446,6 +453,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--split-tokens", type=int, default=0)
+    ap.add_argument("--num-q-heads", type=int, default=0,
+                    help="override the query-head count (the KV heads stay): 64 or 48 over 8 KV heads give the "
+                         "GQA groups of the paper's Qwen3-32B and InternLM2.5-20B")
     ap.add_argument("--num-cand", type=int, default=0,
                     help="override the candidate count of every request (1 = plain decode: 4 rows per KV head)")
     ap.add_argument("--mfma-min-rows", type=int, default=0,
@@ -503,8 +513,9 @@ def main() -> int:
         return 0
     ss.load()
     w = W.workload(args.config)
-    if args.num_cand > 0:
-        w = W.custom(w.hist_len, [args.num_cand] * w.B, num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads,
+    if args.num_cand > 0 or args.num_q_heads > 0:
+        w = W.custom(w.hist_len, [args.num_cand] * w.B if args.num_cand > 0 else w.num_cand,
+                     num_q_heads=args.num_q_heads or w.num_q_heads, num_kv_heads=w.num_kv_heads,
                      head_dim=w.head_dim, chunk_tokens=w.chunk_tokens, cfg_id=args.config)
     log(f"bench: config {args.config} ({w.name}): generating inputs on the GPU")
     layout = {"token": ss.SS_KV_TOKEN_MAJOR, "head": ss.SS_KV_HEAD_MAJOR, "head-kv": ss.SS_KV_HEAD_MAJOR_KV}[args.kv_layout]
@@ -593,7 +604,7 @@ def main() -> int:
             "wall_s_timed": round(wall, 4),
         },
         "roofline": {
-            "kernel": f"chunk_attn (history kernel, two-block MFMA units; one launch over {batch} chunk(s))",
+            "kernel": f"chunk_attn (history kernel, {unit_blocks(w)} MFMA units; one launch over {batch} chunk(s))",
             "bound": "hbm",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,

@@ -58,7 +58,7 @@ typedef int32_t ss_status;
 enum {
   SS_OK = 0,
   SS_ERR_INVALID_ARGUMENT = -1, /* null/misaligned pointer, bad size or count */
-  SS_ERR_UNSUPPORTED = -2,      /* valid but not built: head_dim != 128, rows per KV head > 32 */
+  SS_ERR_UNSUPPORTED = -2,      /* valid but not built: head_dim != 128, rows per KV head > 64 */
   SS_ERR_BAD_STATE = -3,        /* call out of order for this round */
   SS_ERR_NOT_PINNED = -4,       /* upload source is not pinned (page-locked) host memory */
   SS_ERR_WORKSPACE = -5,        /* workspace null, misaligned or too small */
@@ -68,8 +68,11 @@ enum {
 /* Largest candidate count per request (k_b + 1).  The paper's widths are
  * q in {2, 4, 6, 8} (Sec. 5.1). */
 #define SS_MAX_CANDIDATES 8
-/* Rows that share one KV head, n_b * Hq / Hkv, must not exceed this. */
-#define SS_MAX_ROWS_PER_KV_HEAD 32
+/* Rows that share one KV head, n_b * Hq / Hkv, must not exceed this (64
+ * covers GQA groups of 8 query heads at the paper's largest width, q = 8).
+ * A history call with a request of more than 32 such rows runs on a kernel
+ * variant that holds one workgroup per CU. */
+#define SS_MAX_ROWS_PER_KV_HEAD 64
 
 typedef struct {
   int32_t num_requests;     /* B >= 1: one Cohort (Sec. 4.2, Cohort batching)  */

@@ -241,11 +241,13 @@ struct Plan {
 };
 
 // Kernel body of request b's units: VALU for few rows per KV head when the
-// round asks for it, else MFMA with one or two 16-row blocks.
+// round asks for it, else MFMA with one to four 16-row blocks (three or four
+// only on the wide kernel, which a launch with such a unit runs on).
 int kind_of(const ss_round *r, int b) {
   const int min_rows = r->mfma_min_rows > 0 ? r->mfma_min_rows : kDefaultMfmaMinRows;
   const int M = r->n_cand[b] * r->G;
-  return (M < min_rows && M <= ss::kMaxValuRows) ? ss::kUnitValu : (M <= 16) ? ss::kUnitMfma1 : ss::kUnitMfma2;
+  if (M < min_rows && M <= ss::kMaxValuRows) return ss::kUnitValu;
+  return M <= 16 ? ss::kUnitMfma1 : M <= 32 ? ss::kUnitMfma2 : M <= 48 ? ss::kUnitMfma3 : ss::kUnitMfma4;
 }
 
 // Split this call's tokens into W shares.  The requests' tokens (each

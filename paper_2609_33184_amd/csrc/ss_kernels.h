@@ -17,7 +17,7 @@ constexpr int kTile = 32;           // history tokens per wave iteration
 constexpr int kWaves = 4;           // waves per workgroup of the chunk kernels
 constexpr int kMaxCand = 8;         // candidates per request (k_b + 1)
 constexpr int kMaxValuRows = 4;     // rows per KV head the VALU chunk kernel handles
-constexpr int kMaxRows = 32;        // rows per KV head the MFMA chunk kernel handles
+constexpr int kMaxRows = 64;        // rows per KV head the MFMA chunk kernels handle
 constexpr int kClaimCounters = 64;  // balanced history launches per round (one claim counter each)
 
 // Unit kinds: the chunk kernel body that attends a unit (rows per KV head
@@ -25,6 +25,8 @@ constexpr int kClaimCounters = 64;  // balanced history launches per round (one 
 constexpr int kUnitValu = 0;
 constexpr int kUnitMfma1 = 1;
 constexpr int kUnitMfma2 = 2;
+constexpr int kUnitMfma3 = 3;       // wide units: only the one-workgroup-per-CU kernel runs them
+constexpr int kUnitMfma4 = 4;
 
 // Item flag: the slot has not been written in this round yet, so the kernel
 // stores its result instead of merging with (uninitialised) workspace.
@@ -94,7 +96,7 @@ struct ChunkParamsT : ChunkHeader {
   static constexpr int kItems = MaxItems;
   static constexpr int kWgs = MaxWgs;
   // unit u = items [units[u] & 0xffff, + ((units[u] >> 16) & 0xff)), 1..kMaxChain
-  // items, attended by the body units[u] >> 24 (kUnitValu / kUnitMfma1 / kUnitMfma2)
+  // items, attended by the body units[u] >> 24 (kUnitValu / kUnitMfma1..4)
   uint32_t units[MaxUnits];
   // workgroup w (of every KV head) attends units [wg_first[w], wg_first[w + 1]) in order
   uint16_t wg_first[MaxWgs + 1];

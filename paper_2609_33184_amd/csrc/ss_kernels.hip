@@ -91,8 +91,9 @@ __device__ __forceinline__ int global_row(const P &p, const Item &it, int g, int
 template <int ROWS, typename P>
 __device__ __forceinline__ void fold_into_slot(const P &p, const Item &it, int g, int M, int tx,
                                                const float *aw, const float *mw, const float *lw) {
-  // SEGS threads per row, SEGLEN (a multiple of 4) values each
-  constexpr int SEGS = (256 / ROWS) < 32 ? (256 / ROWS) : 32;
+  // SEGS threads per row (the largest power of two with SEGS * ROWS <= 256,
+  // at most 32), SEGLEN (a multiple of 4) values each
+  constexpr int SEGS = (256 / ROWS) >= 32 ? 32 : (256 / ROWS) >= 16 ? 16 : (256 / ROWS) >= 8 ? 8 : 4;
   constexpr int SEGLEN = kHeadDim / SEGS;
   static_assert(SEGLEN % 4 == 0 && SEGS * ROWS <= 256, "fold layout");
   const int r = tx / SEGS;
@@ -649,6 +650,10 @@ __device__ __forceinline__ void valu_unit(const P &p, float *smem, int i0, int n
 constexpr int kValuLdsBytes = kWaves * kMaxValuRows * (kAwPitch + 2) * 4;
 constexpr int kChunkLdsBytes = MfmaLds<2>::kBytes > kValuLdsBytes ? MfmaLds<2>::kBytes : kValuLdsBytes;
 static_assert(MfmaLds<1>::kBytes <= kChunkLdsBytes, "LDS sizes");
+// the wide kernel (one workgroup per CU) also runs 3- and 4-block units
+constexpr int kWideLdsBytes = MfmaLds<4>::kBytes;
+static_assert(MfmaLds<3>::kBytes <= kWideLdsBytes && kChunkLdsBytes <= kWideLdsBytes && kWideLdsBytes <= 160 * 1024,
+              "LDS sizes");
 
 // ---------------------------------------------------------------------------
 // History kernel: one launch for every unit of a call.  Workgroup =
@@ -667,9 +672,9 @@ static_assert(MfmaLds<1>::kBytes <= kChunkLdsBytes, "LDS sizes");
 // until none is left, whatever its own head; each tail unit still owns a
 // fixed state slot, so the result does not depend on who attends it.
 // ---------------------------------------------------------------------------
-template <typename P>
-__global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[kChunkLdsBytes];
+template <bool Wide, typename P>
+__global__ void __launch_bounds__(256, Wide ? 1 : 2) chunk_attn(const P p) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[Wide ? kWideLdsBytes : kChunkLdsBytes];
   __shared__ int claim_sh;
   const int u0 = p.wg_first[blockIdx.y];
   const int u1 = p.wg_first[blockIdx.y + 1];
@@ -704,6 +709,16 @@ __global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
     const int i0 = unit & 0xffff;
     const int nit = (unit >> 16) & 0xff;
     const int kind = unit >> 24;
+    if constexpr (Wide) {
+      if (kind == kUnitMfma4) {
+        mfma_unit<4>(p, smem, i0, nit, tx, g);
+        continue;
+      }
+      if (kind == kUnitMfma3) {
+        mfma_unit<3>(p, smem, i0, nit, tx, g);
+        continue;
+      }
+    }
     if (kind == kUnitMfma2)
       mfma_unit<2>(p, smem, i0, nit, tx, g);
     else if (kind == kUnitMfma1)
@@ -838,27 +853,35 @@ using ChunkSmall = ChunkParamsT<128, 256, 128>;
 using ChunkMedium = ChunkParamsT<512, 1024, 256>;
 using FinalSmall = FinalParamsT<64>;
 
-template <typename D>
+template <bool Wide, typename D>
 hipError_t launch_chunk_as(const ChunkParams &p, hipStream_t s) {
   static thread_local D d;
   static_cast<ChunkHeader &>(d) = p;
   std::memcpy(d.units, p.units, sizeof(uint32_t) * p.num_units);
   std::memcpy(d.wg_first, p.wg_first, sizeof(uint16_t) * (p.num_wgs + 1));
   std::memcpy(d.items, p.items, sizeof(Item) * p.num_items);
-  hipLaunchKernelGGL(chunk_attn<D>, dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, d);
+  hipLaunchKernelGGL((chunk_attn<Wide, D>), dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, d);
+  return hipGetLastError();
+}
+
+template <bool Wide>
+hipError_t launch_chunk_sized(const ChunkParams &p, hipStream_t s) {
+  auto fits = [&](int units, int items, int wgs) {
+    return p.num_units <= units && p.num_items <= items && p.num_wgs <= wgs;
+  };
+  if (fits(ChunkSmall::kUnits, ChunkSmall::kItems, ChunkSmall::kWgs)) return launch_chunk_as<Wide, ChunkSmall>(p, s);
+  if (fits(ChunkMedium::kUnits, ChunkMedium::kItems, ChunkMedium::kWgs)) return launch_chunk_as<Wide, ChunkMedium>(p, s);
+  hipLaunchKernelGGL((chunk_attn<Wide, ChunkParams>), dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_chunk(const ChunkParams &p, hipStream_t s) {
-  auto fits = [&](int units, int items, int wgs) {
-    return p.num_units <= units && p.num_items <= items && p.num_wgs <= wgs;
-  };
-  if (fits(ChunkSmall::kUnits, ChunkSmall::kItems, ChunkSmall::kWgs)) return launch_chunk_as<ChunkSmall>(p, s);
-  if (fits(ChunkMedium::kUnits, ChunkMedium::kItems, ChunkMedium::kWgs)) return launch_chunk_as<ChunkMedium>(p, s);
-  hipLaunchKernelGGL(chunk_attn<ChunkParams>, dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, p);
-  return hipGetLastError();
+  // a launch with any unit of more than two 16-row blocks runs on the wide kernel
+  for (int u = 0; u < p.num_units; ++u)
+    if ((int)(p.units[u] >> 24) >= kUnitMfma3) return launch_chunk_sized<true>(p, s);
+  return launch_chunk_sized<false>(p, s);
 }
 
 hipError_t launch_clear_claims(uint32_t *counters, int n, hipStream_t s) {

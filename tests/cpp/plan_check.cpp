@@ -121,7 +121,7 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
       for (int bb = 0; bb < B; ++bb) if (off_rows[bb] == it.q_row0) b = bb;
       CHECK(b >= 0, "q_row0");
       const int M = it.n_cand * G;
-      const int want_kind = (M < (mfma_min_rows ? mfma_min_rows : 1) && M <= 4) ? 0 : (M <= 16 ? 1 : 2);
+      const int want_kind = (M < (mfma_min_rows ? mfma_min_rows : 1) && M <= 4) ? 0 : (M + 15) / 16;
       CHECK(kind == want_kind, "unit kind %d want %d (M=%d)", kind, want_kind, M);
       int ntiles = 0;
       long toks = 0;
@@ -245,6 +245,8 @@ int main() {
       scenario("config4-like ragged batched 16", 64, 32, 8, n4, h4, 4096, 0, layout, 16, 0, 0, 1);
       scenario("config4-like ragged per-chunk", 64, 32, 8, n4, h4, 4096, 0, layout, 1, 0, 0, -1);
     }
+    scenario("64q/8kv x 8 candidates (64 rows), batched", 16, 64, 8, std::vector<int>(16, 8), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 1);
+    scenario("48q/8kv ragged candidates, per-chunk", 12, 48, 8, {1, 8, 3, 6, 2, 7, 8, 5, 4, 1, 6, 8}, std::vector<int>(12, 9000), 2048, 0, layout, 1);
     scenario("config2 per-chunk (no tail: small shares)", 1, 32, 8, {5}, {16384}, 2048, 0, layout, 8, 0, 0, 0);
     scenario("config5 batched 16", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 16);
     scenario("many units (8192 chains)", 256, 8, 2, std::vector<int>(256, 3), std::vector<int>(256, 4096), 512, 128, layout, 8);
@@ -258,7 +260,8 @@ int main() {
       int nch = 0; for (int x : h) nch = std::max(nch, (x + S - 1) / S);
       if (nch == 0) continue;
       const int batch = 1 + rng() % 32;
-      const int hq = (rng() % 2) ? 32 : 8, hkv = hq == 32 ? 8 : 2;
+      const int hsel = rng() % 4;   // GQA groups of 4, 4, 8 and 6 query heads
+      const int hq = hsel == 0 ? 32 : hsel == 1 ? 8 : hsel == 2 ? 64 : 48, hkv = hsel == 1 ? 2 : 8;
       char nm[64]; snprintf(nm, sizeof nm, "random %d B=%d S=%d split=%d batch=%d", rep, B, S, split, batch);
       const int bal = (rng() % 4 == 0) ? -1 : (rng() % 2 ? 0 : (int)(1 + rng() % 500));
       scenario(nm, B, hq, hkv, nc, h, S, split, layout, batch, (int)(rng() % 6), bal);

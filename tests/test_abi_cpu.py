@@ -75,7 +75,7 @@ def test_workspace_bytes_and_descriptor_validation(lib):
         (ss.make_desc([5], 8, 2, head_dim=64), "head_dim"),
         (ss.make_desc([0], 8, 2), "num_cand"),
         (ss.make_desc([9], 8, 2), "num_cand"),
-        (ss.make_desc([8], 64, 8), "rows per KV head"),                  # 8 * 8 = 64 > 32
+        (ss.make_desc([8], 72, 8), "rows per KV head"),                  # 8 * 9 = 72 > 64
         (ss.make_desc([4], 8, 2, softmax_scale=-1.0), "softmax_scale"),
         (ss.make_desc([4], 8, 2, softmax_scale=float("inf")), "softmax_scale"),
         (ss.make_desc([4], 8, 2, split_tokens=48), "split_tokens"),

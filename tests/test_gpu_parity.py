@@ -145,6 +145,8 @@ def test_small_edge_cases(stream):
         ([257, 513], [4, 2], 64, 8),     # G = 8: 32 rows per KV head
         ([700, 64, 1], [4, 1, 2], 8, 1), # Hkv = 1 (multi-query): 8..32 rows per KV head
         ([5], [8], 4, 1),                # history shorter than the candidate group
+        ([257, 513, 0], [8, 5, 6], 64, 8),  # G = 8: 64, 40, 48 rows per KV head (wide kernel)
+        ([90, 33], [8, 1], 48, 8),          # G = 6: 48 and 6 rows in one launch
     ]
     for k, (lens, cands, hq, hkv) in enumerate(cases):
         w = W.custom(lens, cands, num_q_heads=hq, num_kv_heads=hkv, chunk_tokens=256, seed_base=40 + k)
@@ -246,3 +248,32 @@ def test_graph_replay_matches_eager(stream):
         del g
         if cfg == 4:
             check_sampled(w, b.out, b.lse, [(7, 2)], what="config4 after replays (eager per-chunk round)")
+
+
+@pytest.mark.parametrize("hq", [48, 64], ids=["G6", "G8"])
+def test_wide_query_groups(stream, hq):
+    """GQA groups of 6 and 8 query heads over 8 KV heads (the shapes of the
+    paper's InternLM2.5-20B and Qwen3-32B targets) at widths up to 8: up to
+    48 and 64 rows per KV head, 3- and 4-block units on the wide kernel, in
+    launches that mix them with 1- and 2-block units.  Every output against
+    the oracle, per-chunk and batched calls, all three chunk layouts."""
+    w = W.custom([3000, 1500, 4100, 700], [8, 2, 6, 5], num_q_heads=hq, num_kv_heads=8, chunk_tokens=1024,
+                 seed_base=70 + hq)
+    for layout in LAYOUTS:
+        for batch in (1, w.num_chunks):
+            print(f"Hq={hq}/8 rows per KV head {[n * hq // 8 for n in w.num_cand]} layout={layout} batch={batch}",
+                  flush=True)
+            b = _run(w, stream, kv_layout=layout, batch=batch)
+            _full_check(w, b, f"wide Hq={hq} layout={layout} batch={batch}")
+
+
+def test_wide_query_groups_full_size(stream):
+    """16 requests x 32768 history tokens, 64 query / 8 KV heads, 8
+    candidates: 64 rows per KV head, one batched call over 8 chunks on the
+    wide kernel with the balancing tail; sampled groups against the oracle."""
+    base = W.workload(3)
+    w = W.custom(base.hist_len, [8] * base.B, num_q_heads=64, num_kv_heads=8, chunk_tokens=base.chunk_tokens,
+                 cfg_id=3)
+    print("16 x 32768 tokens, 64q/8kv, 8 candidates, one batched call", flush=True)
+    b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR, batch=w.num_chunks)
+    check_sampled(w, b.out, b.lse, [(0, 0), (7, 3), (15, 7)], what="64q/8kv config3 shape")
