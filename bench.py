@@ -473,7 +473,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-streamed", action="store_true")
     ap.add_argument("--streamed-only", action="store_true",
-                    help="only the streamed round (for memory-copy profiles of the host link)")
+                    help="only the streamed round, timed with HIP events")
+    ap.add_argument("--streamed-trace", action="store_true",
+                    help="only --steps streamed rounds, nothing timed in-process (for rocprofv3 memory-copy traces)")
     ap.add_argument("--cpu-sample-requests", type=int, default=16,
                     help="requests of the workload the fp64 oracle is timed on (16 = all of config 3, ~10 s)")
     ap.add_argument("--per-launch-only", action="store_true",
@@ -519,6 +521,18 @@ def main() -> int:
                      head_dim=w.head_dim, chunk_tokens=w.chunk_tokens, cfg_id=args.config)
     log(f"bench: config {args.config} ({w.name}): generating inputs on the GPU")
     layout = {"token": ss.SS_KV_TOKEN_MAJOR, "head": ss.SS_KV_HEAD_MAJOR, "head-kv": ss.SS_KV_HEAD_MAJOR_KV}[args.kv_layout]
+    if args.streamed_trace:
+        b = H.RoundBuffers(w, kv_layout=layout, balance_permille=args.balance_permille)
+        host = H.HostHistory(w, kv_layout=layout)
+        pipe = H.Pipeline(host.max_chunk_bytes())
+        stream = torch.cuda.Stream()
+        for r in range(max(1, args.steps)):
+            H.run_round_streamed(b, host, pipe, stream.cuda_stream)
+        torch.cuda.synchronize()
+        pipe.close()
+        print(json.dumps({"streamed_trace": {"workload": w.name, "rounds": max(1, args.steps),
+                                             "h2d_bytes_per_round": host.total_bytes}}), flush=True)
+        return 0
     b = H.RoundBuffers(w, split_tokens=args.split_tokens, kv_layout=layout, mfma_min_rows=args.mfma_min_rows,
                        balance_permille=args.balance_permille)
     chunks = H.hbm_history(w, kv_layout=layout)
@@ -651,4 +665,8 @@ def main() -> int:
 
 
 if __name__ == "__main__":
-    sys.exit(main())
+    # a zero status ends the script normally: rocprofv3's memory-copy tracer
+    # crashes in its exit handlers when the process ends through sys.exit(0)
+    _rc = main()
+    if _rc:
+        sys.exit(_rc)
