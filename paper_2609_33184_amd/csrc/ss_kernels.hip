@@ -660,8 +660,10 @@ static_assert(MfmaLds<3>::kBytes <= kWideLdsBytes && kChunkLdsBytes <= kWideLdsB
 // (kv head, w) = (blockIdx.x, blockIdx.y) first attends the units of its own
 // list in order (the host gives every workgroup an equal share of the
 // call's tokens, which may span several requests); each unit's kind selects
-// the body: MFMA with two or one 16-row blocks, or the VALU path for <= 4
-// rows (when the round asks for it).  The heads are the fast grid dimension:
+// the body: MFMA with two or one 16-row blocks (three or four on the wide
+// instantiation, one workgroup per CU, which a launch with such a unit runs
+// on), or the VALU path for <= 4 rows (when the round asks for it).  The
+// heads are the fast grid dimension:
 // with 8 KV heads the round-robin placement gives every XCD one head of
 // every workgroup's share.
 //
