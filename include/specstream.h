@@ -71,7 +71,8 @@ enum {
 /* Rows that share one KV head, n_b * Hq / Hkv, must not exceed this (64
  * covers GQA groups of 8 query heads at the paper's largest width, q = 8).
  * A history call with a request of more than 32 such rows runs on a kernel
- * variant that holds one workgroup per CU. */
+ * variant in which each wave attends every tile for 16 of the rows, with
+ * two workgroups per CU. */
 #define SS_MAX_ROWS_PER_KV_HEAD 64
 
 typedef struct {
@@ -87,7 +88,9 @@ typedef struct {
                                split into equal shares of about this many,
                                one per workgroup and KV head; 0 = automatic
                                (one workgroup per CU, two per CU for calls
-                               whose shares would be below 2048 tokens);
+                               whose shares would be below 2048 tokens or
+                               with a request of more than 32 rows per KV
+                               head);
                                else a multiple of 32                           */
   int32_t mfma_min_rows;    /* rows per KV head (n_b * G) from which the bf16
                                MFMA path is used; fewer (at most 4) use the

@@ -242,7 +242,8 @@ struct Plan {
 
 // Kernel body of request b's units: VALU for few rows per KV head when the
 // round asks for it, else MFMA with one to four 16-row blocks (three or four
-// only on the wide kernel, which a launch with such a unit runs on).
+// only on the wide kernel, which a launch with such a unit runs on, as
+// row-split units).
 int kind_of(const ss_round *r, int b) {
   const int min_rows = r->mfma_min_rows > 0 ? r->mfma_min_rows : kDefaultMfmaMinRows;
   const int M = r->n_cand[b] * r->G;
@@ -383,8 +384,15 @@ ss_status plan_chunks(const ss_round *r, int nchunks, const int32_t *len, const 
   if (r->split_tokens > 0) {
     W = (total + r->split_tokens - 1) / r->split_tokens;
   } else {
+    // Row-split units (three or four 16-row blocks) also get two workgroups
+    // per CU: each of their tile steps is a barrier-bound chain of LDS and
+    // MFMA latencies, which a second workgroup on the CU overlaps.
+    bool wide = false;
+    for (int c = 0; c < nchunks && !wide; ++c)
+      for (int b = 0; b < r->B && !wide; ++b)
+        wide = len[(size_t)c * r->B + b] > 0 && kind_of(r, b) >= ss::kUnitMfma3;
     W = std::max<long>(1, kTargetWorkgroups / r->Hkv);
-    if (total / W < kSmallShare) W = std::max<long>(1, 2 * kTargetWorkgroups / r->Hkv);
+    if (total / W < kSmallShare || wide) W = std::max<long>(1, 2 * kTargetWorkgroups / r->Hkv);
     W = std::min(W, std::max<long>(1, total / kMinPiece));
   }
   W = std::max<long>(1, std::min<long>(W, total));

@@ -25,7 +25,7 @@ constexpr int kClaimCounters = 64;  // balanced history launches per round (one 
 constexpr int kUnitValu = 0;
 constexpr int kUnitMfma1 = 1;
 constexpr int kUnitMfma2 = 2;
-constexpr int kUnitMfma3 = 3;       // wide units: only the one-workgroup-per-CU kernel runs them
+constexpr int kUnitMfma3 = 3;       // wide units (row-split body): only the wide kernel runs them
 constexpr int kUnitMfma4 = 4;
 
 // Item flag: the slot has not been written in this round yet, so the kernel

@@ -21,6 +21,7 @@
 
 #include "ss_kernels.h"
 
+#include <cstddef>
 #include <cstring>
 
 #include <math.h>
@@ -201,6 +202,16 @@ constexpr int kTileBytes = kTile * kRowBytes;    // 8 KiB per K or V tile
 
 __device__ __forceinline__ int tiles_of(const Item &it) { return (it.tok_count + kTile - 1) / kTile; }
 
+// Chunk-table index of an item.  The item is read as whole dwords: a
+// byte-sized read of a kernel argument becomes a vector memory load, and the
+// wait for it would also wait for every K/V load in flight.
+__device__ __forceinline__ int item_chunk(const Item &it) {
+  uint32_t w[4];
+  __builtin_memcpy(w, &it, sizeof w);
+  return (int)((w[3] >> 8) & 0xffu);
+}
+static_assert(offsetof(Item, chunk) == 13, "Item layout");
+
 // Buffer resource over item `it`'s rows of KV head g in chunk table `tab`
 // (p.k or p.v): loads past the item's last token return zero, so no
 // clamping is needed.  Offsets are 32-bit (the host keeps an item below
@@ -208,9 +219,10 @@ __device__ __forceinline__ int tiles_of(const Item &it) { return (it.tok_count +
 template <typename P>
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t item_rsrc(const P &p, const Item &it, int g,
                                                             const uint16_t *const *tab) {
+  const int chunk = item_chunk(it);
   const uint32_t nrec = (uint32_t)(it.tok_count - 1) * (p.tok_stride * 2) + kRowBytes;
-  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride[it.chunk];
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(tab[it.chunk] + first), (short)0, (int)nrec,
+  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride[chunk];
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(tab[chunk] + first), (short)0, (int)nrec,
                                            kBufferFlags);
 }
 
@@ -472,6 +484,247 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i
 }
 
 // ---------------------------------------------------------------------------
+// Row-split MFMA body for wide query groups (33..64 rows per KV head).  Wave
+// w owns rows 16w .. 16w+15 and attends every tile of the unit, so no
+// cross-wave merge is needed: a wave holds one 16-row block of accumulators
+// and its query operand in registers, and the wide kernel keeps two
+// workgroups per CU.  The four waves stage each 32-token tile together
+// (wave w loads tokens 8w .. 8w+7 of K and of V) into one of two LDS tile
+// buffers, with one workgroup barrier per tile; each wave keeps the loads of
+// the next kRowsAhead tiles in flight in registers.  Per tile a wave runs
+// the one-block math of the body above (same LDS swizzle and operand
+// layouts): S^T = K Q^T, the online softmax, O^T += V^T P^T with P as hi + lo.
+//
+// Tile t is staged in buffer t % 2.  A wave writes buffer t % 2 only after
+// the barrier of tile t - 1, which every wave reaches after attending tile
+// t - 2, the buffer's previous contents; the barrier of tile t then makes
+// the whole tile visible.  Every wave runs the same number of barriers:
+// tiles past the unit's end (up to kRowsAhead - 1 of them) are loaded from
+// an empty buffer resource, which reads zeros, staged and not attended.
+// ---------------------------------------------------------------------------
+constexpr int kRowsAhead = 4;                      // tiles of loads in flight per wave
+constexpr int kRowsLdsBytes = 2 * 2 * kTileBytes;  // two K + V tile buffers
+
+template <typename P>
+__device__ __forceinline__ void rows_unit(const P &p, unsigned char *smem, int i0, int nit, int tx, int g) {
+  const int w = __builtin_amdgcn_readfirstlane(tx >> 6);   // wave-uniform
+  const int lane = tx & 63;
+  const int lr = lane & 15;
+  const int lq = lane >> 4;
+  const Item it = p.items[i0];          // request, slot and flags of the whole chain
+  const int M = it.n_cand * p.G;
+  const bool active = 16 * w < M;       // wave-uniform: the wave has rows
+  int ntiles = 0;
+  for (int k = 0; k < nit; ++k) ntiles += tiles_of(p.items[i0 + k]);
+
+  const uint32_t stride_b = p.tok_stride * 2;                // bytes between tokens
+  const uint32_t voff = (8 * w + lq) * stride_b + 16 * lr;     // token 8w + lq, chunk lr
+  const float sl2 = p.scale_log2;
+
+  // Q^T operand (B[k = d][j = row]) of row 16w + lr, k-step s: d-chunk
+  // 4s + lq.  A padding row (>= M) gets an offset past the end: zeros.
+  const int row = 16 * w + lr;
+  const __amdgpu_buffer_rsrc_t qrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t *>(p.q), (short)0, (int)((uint32_t)p.st.R * kRowBytes), kBufferFlags);
+  const uint32_t qoff = row < M ? (uint32_t)global_row(p, it, g, row) * kRowBytes + 16 * lq : 0x80000000u;
+  bf16x8_t qop[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    qop[s] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 64 * s, 0, 0));
+
+  // loads of tile t: K rows 8w + lq and 8w + 4 + lq, then the same V rows.
+  // Tiles are requested in order; the resources of the current item are
+  // kept and rebuilt only when the tile moves on to the next item, so a
+  // step issues its loads without a chain of dependent argument reads.
+  // The loads themselves are unconditional (a conditional load would make
+  // the compiler wait for every outstanding one): past the unit's last tile
+  // they go through an empty resource.
+  const __amdgpu_buffer_rsrc_t empty =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.q), (short)0, 0, kBufferFlags);
+  int lk = 0, lbase = 0, lend = tiles_of(p.items[i0]);
+  __amdgpu_buffer_rsrc_t lkrs = item_rsrc(p, p.items[i0], g, p.k);
+  __amdgpu_buffer_rsrc_t lvrs = item_rsrc(p, p.items[i0], g, p.v);
+  auto issue = [&](u32x4_t (&d)[4], int t) {
+    if (t >= lend && t < ntiles) {
+      while (t >= lend) {
+        lbase = lend;
+        lend += tiles_of(p.items[i0 + ++lk]);
+      }
+      lkrs = item_rsrc(p, p.items[i0 + lk], g, p.k);
+      lvrs = item_rsrc(p, p.items[i0 + lk], g, p.v);
+    }
+    const bool in = t < ntiles;
+    const __amdgpu_buffer_rsrc_t krs = in ? lkrs : empty;
+    const __amdgpu_buffer_rsrc_t vrs = in ? lvrs : empty;
+    const uint32_t o = voff + (uint32_t)(in ? (t - lbase) * kTile : 0) * stride_b;
+    d[0] = __builtin_amdgcn_raw_buffer_load_b128(krs, o, 0, kStreamLoad);
+    d[1] = __builtin_amdgcn_raw_buffer_load_b128(krs, o + 4 * stride_b, 0, kStreamLoad);
+    d[2] = __builtin_amdgcn_raw_buffer_load_b128(vrs, o, 0, kStreamLoad);
+    d[3] = __builtin_amdgcn_raw_buffer_load_b128(vrs, o + 4 * stride_b, 0, kStreamLoad);
+  };
+  auto stage = [&](const u32x4_t (&d)[4], unsigned char *buf) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int t = 8 * w + 4 * j + lq;
+      *reinterpret_cast<u32x4_t *>(buf + t * kRowBytes + 16 * (lr ^ (t & 15))) = d[j];
+      *reinterpret_cast<u32x4_t *>(buf + kTileBytes + t * kRowBytes + 16 * (lr ^ (2 * (t & 7)))) = d[2 + j];
+    }
+  };
+
+  float m_run = kNegInf, l_run = 0.f;
+  f32x4_t acc[8];
+#pragma unroll
+  for (int db = 0; db < 8; ++db) acc[db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int vrow = 4 * lq + (lr >> 2);
+  const int vrd = vrow * kRowBytes + 8 * (lr & 1);
+  const int vsw = 2 * (vrow & 7);
+  const int vc0 = (lr & 3) >> 1;
+  // item of the tile being attended: index, first tile, end tile, tokens
+  int ck = 0, cbase = 0, cend = lend, count = p.items[i0].tok_count;
+
+  // attend staged tile t (tokens [tb, tb + 32) of an item with `count` tokens)
+  auto attend = [&](const unsigned char *buf, int t) {
+    if (t >= cend) {
+      while (t >= cend) {
+        cbase = cend;
+        cend += tiles_of(p.items[i0 + ++ck]);
+      }
+      count = p.items[i0 + ck].tok_count;
+    }
+    const int tb = (t - cbase) * kTile;
+    const unsigned char *ks = buf;
+    const unsigned char *vs = buf + kTileBytes;
+    f32x4_t sacc[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int tk = 16 * u + lr;
+      f32x4_t c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const bf16x8_t kop = *reinterpret_cast<const bf16x8_t *>(ks + tk * kRowBytes + 16 * ((4 * s + lq) ^ lr));
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[s], c, 0, 0, 0);
+      }
+      sacc[u] = c;
+    }
+    // the V^T operands go out now, so their LDS latency hides behind the softmax
+    bf16x8_t vop[8];
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      const int off = vrd + 16 * ((2 * db + vc0) ^ vsw);
+      const s16x4_t v0 = lds_read_tr16(vs + off);
+      const s16x4_t v1 = lds_read_tr16(vs + off + 16 * kRowBytes);
+      vop[db] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+
+    __builtin_amdgcn_sched_barrier(0);
+
+    // Scores stay unscaled up to the exponent: the row maximum of the raw
+    // scores times sigma log2(e) (> 0) is the maximum of the scaled ones,
+    // and each weight is 2^(x sigma log2(e) - m) with one fma.  Only an
+    // item's last, partial tile needs the token mask.
+    float x[8];
+    float mx = kNegInf;
+    if (tb + kTile <= count) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          x[4 * u + r] = sacc[u][r];
+          mx = fmaxf(mx, sacc[u][r]);
+        }
+    } else {
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int tt = tb + 16 * u + 4 * lq + r;
+          const float v = tt < count ? sacc[u][r] : kNegInf;
+          x[4 * u + r] = v;
+          mx = fmaxf(mx, v);
+        }
+    }
+    const float mn = fmaxf(m_run, xgroup_max(mx) * sl2);
+    // Eq. 14's rescale, only when some row's maximum rose (elsewhere the
+    // factor is exactly 1)
+    if (__builtin_amdgcn_ballot_w64(mn > m_run)) {
+      const float alpha = exp2_fast(m_run - mn);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < 8; ++db) acc[db] *= alpha;
+      m_run = mn;
+    }
+    bf16x8_t phi, plo;
+    float ls = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float pe = exp2_fast(__builtin_fmaf(x[e], sl2, -mn));
+      const __bf16 h = (__bf16)pe;
+      const float hf = (float)h;
+      const __bf16 lo = (__bf16)(pe - hf);
+      phi[e] = h;
+      plo[e] = lo;
+      ls += hf + (float)lo;
+    }
+    l_run += ls;
+
+    __builtin_amdgcn_sched_barrier(0);
+
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[db], phi, acc[db], 0, 0, 0);
+      acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[db], plo, acc[db], 0, 0, 0);
+    }
+  };
+
+  u32x4_t ld[kRowsAhead][4];
+#pragma unroll
+  for (int i = 0; i < kRowsAhead; ++i) issue(ld[i], i);
+  for (int t0 = 0; t0 < ntiles; t0 += kRowsAhead) {
+#pragma unroll
+    for (int i = 0; i < kRowsAhead; ++i) {
+      const int t = t0 + i;
+      unsigned char *buf = smem + (i & 1) * (2 * kTileBytes);
+      stage(ld[i], buf);
+      issue(ld[i], t + kRowsAhead);
+      __syncthreads();
+      if (active && t < ntiles) attend(buf, t);
+    }
+  }
+
+  // the wave's rows -> their slot (Eq. 14 with the slot's state unless the
+  // slot is fresh).  Lane (lr, lq) holds d = 16db + 4lq .. +3 of row 16w + lr.
+  if (!active) return;
+  l_run = xgroup_sum(l_run);
+  if (row >= M) return;
+  const size_t idx = (size_t)it.slot * p.st.R + global_row(p, it, g, row);
+  float *ap = p.st.a + idx * kHeadDim + 4 * lq;
+  if (it.flags & kSlotFresh) {
+#pragma unroll
+    for (int db = 0; db < 8; ++db) *reinterpret_cast<f32x4_t *>(ap + 16 * db) = acc[db];
+    if (lq == 0) {
+      p.st.m[idx] = m_run;
+      p.st.l[idx] = l_run;
+    }
+  } else {
+    const float ms = p.st.m[idx];
+    const float ls = p.st.l[idx];
+    const float mn = fmaxf(ms, m_run);
+    const float alpha = exp2_fast(ms - mn);
+    const float beta = exp2_fast(m_run - mn);
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      f32x4_t o = *reinterpret_cast<const f32x4_t *>(ap + 16 * db);
+      o = alpha * o + beta * acc[db];
+      *reinterpret_cast<f32x4_t *>(ap + 16 * db) = o;
+    }
+    if (lq == 0) {
+      p.st.m[idx] = mn;
+      p.st.l[idx] = alpha * ls + beta * l_run;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // VALU chunk body for sparse query groups (few rows per KV head), used when
 // the round's mfma_min_rows asks for it: fp32 dot products on the vector
 // ALUs, exact fp32 softmax weights.  Lane l: d-chunk
@@ -650,20 +903,17 @@ __device__ __forceinline__ void valu_unit(const P &p, float *smem, int i0, int n
 constexpr int kValuLdsBytes = kWaves * kMaxValuRows * (kAwPitch + 2) * 4;
 constexpr int kChunkLdsBytes = MfmaLds<2>::kBytes > kValuLdsBytes ? MfmaLds<2>::kBytes : kValuLdsBytes;
 static_assert(MfmaLds<1>::kBytes <= kChunkLdsBytes, "LDS sizes");
-// the wide kernel (one workgroup per CU) also runs 3- and 4-block units
-constexpr int kWideLdsBytes = MfmaLds<4>::kBytes;
-static_assert(MfmaLds<3>::kBytes <= kWideLdsBytes && kChunkLdsBytes <= kWideLdsBytes && kWideLdsBytes <= 160 * 1024,
-              "LDS sizes");
+static_assert(kRowsLdsBytes <= kChunkLdsBytes && 2 * kChunkLdsBytes <= 160 * 1024, "LDS sizes");
 
 // ---------------------------------------------------------------------------
 // History kernel: one launch for every unit of a call.  Workgroup =
 // (kv head, w) = (blockIdx.x, blockIdx.y) first attends the units of its own
 // list in order (the host gives every workgroup an equal share of the
 // call's tokens, which may span several requests); each unit's kind selects
-// the body: MFMA with two or one 16-row blocks (three or four on the wide
-// instantiation, one workgroup per CU, which a launch with such a unit runs
-// on), or the VALU path for <= 4 rows (when the round asks for it).  The
-// heads are the fast grid dimension:
+// the body: MFMA with two or one 16-row blocks, the row-split body for
+// three or four (only on the wide instantiation, which a launch with such a
+// unit runs on), or the VALU path for <= 4 rows (when the round asks for
+// it).  The heads are the fast grid dimension:
 // with 8 KV heads the round-robin placement gives every XCD one head of
 // every workgroup's share.
 //
@@ -675,8 +925,8 @@ static_assert(MfmaLds<3>::kBytes <= kWideLdsBytes && kChunkLdsBytes <= kWideLdsB
 // fixed state slot, so the result does not depend on who attends it.
 // ---------------------------------------------------------------------------
 template <bool Wide, typename P>
-__global__ void __launch_bounds__(256, Wide ? 1 : 2) chunk_attn(const P p) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[Wide ? kWideLdsBytes : kChunkLdsBytes];
+__global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kChunkLdsBytes];
   __shared__ int claim_sh;
   const int u0 = p.wg_first[blockIdx.y];
   const int u1 = p.wg_first[blockIdx.y + 1];
@@ -712,12 +962,8 @@ __global__ void __launch_bounds__(256, Wide ? 1 : 2) chunk_attn(const P p) {
     const int nit = (unit >> 16) & 0xff;
     const int kind = unit >> 24;
     if constexpr (Wide) {
-      if (kind == kUnitMfma4) {
-        mfma_unit<4>(p, smem, i0, nit, tx, g);
-        continue;
-      }
-      if (kind == kUnitMfma3) {
-        mfma_unit<3>(p, smem, i0, nit, tx, g);
+      if (kind >= kUnitMfma3) {
+        rows_unit(p, smem, i0, nit, tx, g);
         continue;
       }
     }

@@ -245,7 +245,9 @@ int main() {
       scenario("config4-like ragged batched 16", 64, 32, 8, n4, h4, 4096, 0, layout, 16, 0, 0, 1);
       scenario("config4-like ragged per-chunk", 64, 32, 8, n4, h4, 4096, 0, layout, 1, 0, 0, -1);
     }
-    scenario("64q/8kv x 8 candidates (64 rows), batched", 16, 64, 8, std::vector<int>(16, 8), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 1);
+    // row-split units get two workgroups per CU: 8192-token shares, below the default tail's threshold
+    scenario("64q/8kv x 8 candidates (64 rows), batched", 16, 64, 8, std::vector<int>(16, 8), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 0);
+    scenario("64q/8kv x 8 candidates, batched, tail 100", 16, 64, 8, std::vector<int>(16, 8), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 100, 1);
     scenario("48q/8kv ragged candidates, per-chunk", 12, 48, 8, {1, 8, 3, 6, 2, 7, 8, 5, 4, 1, 6, 8}, std::vector<int>(12, 9000), 2048, 0, layout, 1);
     scenario("config2 per-chunk (no tail: small shares)", 1, 32, 8, {5}, {16384}, 2048, 0, layout, 8, 0, 0, 0);
     scenario("config5 batched 16", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 16);
