@@ -499,10 +499,13 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i
 // the barrier of tile t - 1, which every wave reaches after attending tile
 // t - 2, the buffer's previous contents; the barrier of tile t then makes
 // the whole tile visible.  Every wave runs the same number of barriers:
-// tiles past the unit's end (up to kRowsAhead - 1 of them) are loaded from
-// an empty buffer resource, which reads zeros, staged and not attended.
+// the steps run in groups of kRowsAhead, and a step past the unit's last
+// tile (up to kRowsAhead - 1 of them) stages zeros and attends nothing.
+// Loads for tiles past the end (the last kRowsAhead issued are never
+// staged) go through an empty buffer resource, which reads zeros without
+// touching memory.
 // ---------------------------------------------------------------------------
-constexpr int kRowsAhead = 4;                      // tiles of loads in flight per wave
+constexpr int kRowsAhead = 4;   // tiles of loads in flight per wave; even, so step i of a group uses buffer i % 2
 constexpr int kRowsLdsBytes = 2 * 2 * kTileBytes;  // two K + V tile buffers
 
 template <typename P>
