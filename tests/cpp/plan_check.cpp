@@ -185,7 +185,8 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
 }
 
 static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> ncand, std::vector<int> hist, int S,
-                     int split, int layout, int batch, int mfma_min_rows = 0, int balance = 0, int expect_tail = -1) {
+                     int split, int layout, int batch, int mfma_min_rows = 0, int balance = 0, int expect_tail = -1,
+                     int expect_wgs = -1) {
   const int nch = [&] { int m = 0; for (int h : hist) m = std::max(m, (h + S - 1) / S); return m; }();
   std::vector<std::vector<int>> lens(nch, std::vector<int>(B));
   long maxc = 1;
@@ -212,6 +213,11 @@ static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> 
   ss_round_destroy(r);
   CHECK(g_clears == (g_tail_calls > 0 ? 1 : 0), "%d clears for %d balanced calls", g_clears, g_tail_calls);
   if (expect_tail >= 0) CHECK((g_tail_calls > 0) == (expect_tail > 0), "%s: %d balanced calls", name, g_tail_calls);
+  // workgroups per KV head of the last call's launches
+  if (expect_wgs >= 0)
+    for (auto &rc : g_recs)
+      CHECK((int)rc.wg_first.size() - 1 == expect_wgs, "%s: %d workgroups per KV head, want %d", name,
+            (int)rc.wg_first.size() - 1, expect_wgs);
   printf("%-44s %s (launches in last call: %zu, balanced calls: %d)\n", name, fails == before ? "ok" : "FAILED",
          g_recs.size(), g_tail_calls);
 }
@@ -224,7 +230,8 @@ int main() {
     scenario("config1 split 96", 1, 8, 2, {5}, {4096}, 1024, 96, layout, 1);
     scenario("config1 batched", 1, 8, 2, {5}, {4096}, 1024, 0, layout, 4);
     scenario("config2 per-chunk", 1, 32, 8, {5}, {16384}, 2048, 0, layout, 1);
-    scenario("config3 batched 8", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 1);
+    // one workgroup per CU: 8 KV heads x 32
+    scenario("config3 batched 8", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 1, 32);
     scenario("16 x 16384 batched 4 (no tail: shares of 8192)", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 16384), 4096, 0, layout, 4, 0, 0, 0);
     scenario("16 x 65536 batched 16 (tail)", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 65536), 4096, 0, layout, 16, 0, 0, 1);
     scenario("config3 batched 8, no tail", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, -1, 0);
@@ -245,9 +252,11 @@ int main() {
       scenario("config4-like ragged batched 16", 64, 32, 8, n4, h4, 4096, 0, layout, 16, 0, 0, 1);
       scenario("config4-like ragged per-chunk", 64, 32, 8, n4, h4, 4096, 0, layout, 1, 0, 0, -1);
     }
-    // row-split units get two workgroups per CU: 8192-token shares, below the default tail's threshold
-    scenario("64q/8kv x 8 candidates (64 rows), batched", 16, 64, 8, std::vector<int>(16, 8), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 0);
-    scenario("64q/8kv x 8 candidates, batched, tail 100", 16, 64, 8, std::vector<int>(16, 8), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 100, 1);
+    // row-split units get two workgroups per CU (8 KV heads x 64): 8192-token shares, below the default
+    // tail's threshold
+    scenario("64q/8kv x 8 candidates (64 rows), batched", 16, 64, 8, std::vector<int>(16, 8), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 0, 64);
+    scenario("64q/8kv x 8 candidates, batched, tail 100", 16, 64, 8, std::vector<int>(16, 8), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 100, 1, 64);
+    scenario("64q/8kv x 4 candidates (32 rows), batched", 16, 64, 8, std::vector<int>(16, 4), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 1, 32);
     scenario("48q/8kv ragged candidates, per-chunk", 12, 48, 8, {1, 8, 3, 6, 2, 7, 8, 5, 4, 1, 6, 8}, std::vector<int>(12, 9000), 2048, 0, layout, 1);
     scenario("config2 per-chunk (no tail: small shares)", 1, 32, 8, {5}, {16384}, 2048, 0, layout, 8, 0, 0, 0);
     scenario("config5 batched 16", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 16);
