@@ -271,9 +271,10 @@ def test_wide_query_groups_full_size(stream):
     """16 requests x 32768 history tokens, 64 query / 8 KV heads, 8
     candidates: 64 rows per KV head, one batched call over 8 chunks on the
     wide kernel (row-split units, two workgroups per CU), once as planned by
-    default and once with a balancing tail; sampled groups against the
-    oracle, and the two results within 1e-5 of each other (the two plans
-    split the tokens into different units, so only the rounding differs)."""
+    default and twice with a balancing tail; sampled groups against the
+    oracle, the default and tailed results within 1e-5 of each other (the
+    two plans split the tokens into different units, so only the rounding
+    differs), and the two tailed runs bitwise equal."""
     base = W.workload(3)
     w = W.custom(base.hist_len, [8] * base.B, num_q_heads=64, num_kv_heads=8, chunk_tokens=base.chunk_tokens,
                  cfg_id=3)
@@ -286,3 +287,9 @@ def test_wide_query_groups_full_size(stream):
     check_sampled(w, b.out, b.lse, [(3, 1), (12, 6)], what="64q/8kv config3 shape, balancing tail")
     assert (b.out - out0).abs().max().item() <= 1e-5
     assert (b.lse - lse0).abs().max().item() <= 1e-5
+    # the tail's row-split units go to whichever workgroups claim them, but
+    # each owns its slot: a repeat is bitwise equal
+    out1, lse1 = b.out.clone(), b.lse.clone()
+    del b
+    b = _run(w, stream, kv_layout=ss.SS_KV_HEAD_MAJOR, batch=w.num_chunks, balance_permille=100)
+    assert torch.equal(b.out, out1) and torch.equal(b.lse, lse1)
