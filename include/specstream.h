@@ -30,11 +30,14 @@
  *     multiplies the dot product (1/sqrt(d) in the paper, Sec. 4.2).
  *   - Ownership: the caller owns every buffer, stream and event and keeps
  *     them alive until the enqueued work has finished.  The library never
- *     allocates device memory; its only state is the host handle.
+ *     allocates device memory; its only state is the host handles.
  *   - Asynchrony: calls validate, enqueue on the given stream and return.
- *     A non-OK status means nothing was enqueued by that call (except
- *     SS_ERR_HIP, reported when a launch itself fails).  Device faults
- *     surface at the caller's synchronisation.
+ *     A non-OK status means nothing was enqueued by that call, except
+ *     SS_ERR_HIP, reported when a HIP call itself fails: if part of the
+ *     call's work had already been enqueued, the round (and a pipeline the
+ *     call went through) is marked failed and refuses every later call with
+ *     SS_ERR_BAD_STATE; destroy it.  Device faults surface at the caller's
+ *     synchronisation.
  *   - All calls of one round go to one stream (or are ordered by events);
  *     calls of one round that overlap on different streams race.
  *   - Threading: one host thread per handle at a time.  ss_last_error() is
@@ -62,7 +65,8 @@ enum {
   SS_ERR_BAD_STATE = -3,        /* call out of order for this round */
   SS_ERR_NOT_PINNED = -4,       /* upload source is not pinned (page-locked) host memory */
   SS_ERR_WORKSPACE = -5,        /* workspace null, misaligned or too small */
-  SS_ERR_HIP = -6               /* a HIP runtime call failed (detail in ss_last_error) */
+  SS_ERR_HIP = -6,              /* a HIP runtime call failed (detail in ss_last_error) */
+  SS_ERR_OUT_OF_MEMORY = -7     /* a host allocation of the library failed; nothing was enqueued */
 };
 
 /* Largest candidate count per request (k_b + 1).  The paper's widths are
@@ -111,6 +115,22 @@ typedef struct {
                                shares hold at least 16384 tokens, a value set
                                here from 4096; the result is the same bitwise
                                whichever workgroup attends a unit              */
+  int32_t counters_zeroed;  /* the workspace ends with a block of counters
+                               (the balancing tail's claims, the fused
+                               finalize's per-(request, KV head) counts) that
+                               must be zero when a launch that uses them
+                               starts; every such launch leaves them zero.
+                               0 = the library zeroes the block with a
+                               one-wave kernel before the round's first launch
+                               that uses it.  1 = the caller guarantees it is
+                               zero: the workspace was zero-filled when it was
+                               allocated and has since been written only by
+                               rounds of this library whose work completed
+                               without error (a serving loop reusing one
+                               workspace), so no clear is enqueued.  A block
+                               that is not zero when promised gives wrong
+                               results (never an access outside the
+                               workspace).                                    */
 } ss_round_desc;
 
 /* History chunk layouts (ss_round_desc.kv_layout).  In all, request b's
@@ -124,9 +144,10 @@ typedef struct {
 #define SS_KV_HEAD_MAJOR_KV 2
 
 /* Bytes of device workspace a round with this descriptor needs (fp32
- * online-softmax states of every query row, per split slot, and 256 bytes of
- * claim counters for the balanced history calls).  0 if the descriptor is
- * invalid (see ss_last_error). */
+ * online-softmax states of every query row, per split slot, then the counter
+ * block: 64 words, one of them the balancing tail's claim counter, and one
+ * word per (request, KV head) for the fused finalize).  0 if the descriptor
+ * is invalid (see ss_last_error). */
 size_t ss_round_workspace_bytes(const ss_round_desc *desc);
 
 /* Start a round (paper Sec. 4.2: state (m, l, a) = (-inf, 0, 0) per query and
@@ -135,9 +156,10 @@ size_t ss_round_workspace_bytes(const ss_round_desc *desc);
  * workspace: device, 256-byte aligned, >= ss_round_workspace_bytes(desc);
  * owned by the round until finalize's work has completed.  The empty state
  * is tracked on the host (a split slot is written before it is ever read),
- * so this call enqueues nothing on `stream`; the round's first history call
- * with a balancing tail enqueues a one-wave kernel that zeroes the claim
- * counters before its attention launch.
+ * so this call enqueues nothing on `stream`; unless desc->counters_zeroed is
+ * set, the round's first launch that uses the counter block (a history call
+ * with a balancing tail, or ss_round_finalize_chunks) is preceded by a
+ * one-wave kernel that zeroes it.
  * On success *out receives a new handle (free with ss_round_destroy). */
 ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q,
                         void *workspace, size_t workspace_bytes, hipStream_t stream);
@@ -166,9 +188,9 @@ ss_status ss_upload_chunk(void *dst_device, const void *src_pinned_host, size_t 
 ss_status ss_attend_history_chunk(ss_round *r, const void *k, const void *v, const int32_t *len,
                                   hipEvent_t wait_before, hipEvent_t signal_after, hipStream_t stream);
 
-/* Attend several history chunks in one launch (paper Sec. 4.2: adjacent
- * chunks are grouped into batches to amortise submission, synchronisation
- * and kernel-launch costs).  Same semantics as num_chunks calls of
+/* Attend several history chunks in one launch (paper Sec. 4.2, transfer
+ * batching: one launch serves a group of adjacent chunks, so its fixed
+ * costs are paid once for the group).  Same semantics as num_chunks calls of
  * ss_attend_history_chunk, in any order.  k, v: host arrays [num_chunks] of
  * device chunk pointers (each chunk in the round's kv_layout); len: host
  * [num_chunks][B] token counts; 1 <= num_chunks <= 32.  wait_before and
@@ -192,6 +214,21 @@ ss_status ss_attend_local_candidates(ss_round *r, const void *k_cand, const void
  * (m + ln l).  Requires ss_attend_local_candidates to have been called.
  * After finalize the handle accepts no more calls except destroy. */
 ss_status ss_round_finalize(ss_round *r, float *out, float *lse, hipStream_t stream);
+
+/* The round's last history chunks and its finalize in one launch (paper
+ * Sec. 4.2: the chunks' Eq. 13 / Eq. 14 updates, then the frontier pass and
+ * O = a / l of Eq. 17).  Same result, bitwise, as ss_attend_history_chunks
+ * with the same arguments followed by ss_round_finalize: within the launch,
+ * the unit that completes a (request, KV head) pair's work merges the
+ * pair's slots, attends its frontier and writes its rows of out and lse.
+ * Arguments as for those two calls; requires ss_attend_local_candidates to
+ * have been called; no history call may follow.  signal_after is recorded
+ * after the launch.  A call that does not fit one launch (more than 4096
+ * requests, or more units than one launch's tables hold) runs as the two
+ * calls.  Uses the workspace's counter block (see counters_zeroed). */
+ss_status ss_round_finalize_chunks(ss_round *r, int32_t num_chunks, const void *const *k, const void *const *v,
+                                   const int32_t *len, hipEvent_t wait_before, hipEvent_t signal_after,
+                                   float *out, float *lse, hipStream_t stream);
 
 /* Free the host handle (never device memory).  Null is ignored.  Call it
  * after enqueueing finalize; enqueued work does not use the handle. */
@@ -218,11 +255,10 @@ ss_status ss_pipeline_create(ss_pipeline **out, void *staging0, void *staging1, 
 ss_status ss_pipeline_attend_chunk(ss_pipeline *p, ss_round *r, const void *host_kv,
                                    const int32_t *len, hipStream_t stream);
 
-/* Transfer batch (paper Sec. 4.2: adjacent chunks are grouped into transfer
- * batches to amortise copy submission, synchronisation and kernel launches):
- * upload num_chunks adjacent history chunks into the next staging slot with
- * one copy and attend them with one launch, as ss_attend_history_chunks
- * does.  host_kv: pinned host memory holding chunk 0's K, chunk 0's V, chunk
+/* Transfer batch (paper Sec. 4.2): num_chunks adjacent history chunks go to
+ * the next staging slot as one copy and are attended by one launch, as
+ * ss_attend_history_chunks does, so the copy's and the launch's fixed costs
+ * are paid once for the group.  host_kv: pinned host memory holding chunk 0's K, chunk 0's V, chunk
  * 1's K, ... contiguously (each in the round's kv_layout; with
  * SS_KV_HEAD_MAJOR_KV each chunk's one K-and-V buffer); len: host
  * [num_chunks][B]; 1 <= num_chunks <= 32; the batch must fit slot_bytes. */
@@ -237,10 +273,11 @@ void ss_pipeline_destroy(ss_pipeline *p);
  *   [0, H)  Sealed History       host (pinned memory), streamed as chunks
  *   [H, C)  Active Tail          GPU, committed tokens not yet migrated
  *   [C, L)  Speculative Frontier GPU, candidates awaiting verification
- * Committed tokens older than the tail target T move to the host in blocks
- * of g tokens; H advances only after the copy has completed, and the
- * rejected suffix of the frontier is released on the GPU alone (it never
- * overlaps [0, H), so no host cleanup or cross-device rollback exists). */
+ * Committed tokens more than T behind C move to the host in blocks of g
+ * tokens.  The boundary H moves forward only once a migration's copy is
+ * done (ss_tier_complete).  A rejected suffix of the frontier lies at or
+ * after C >= H, so releasing it touches GPU memory only and never the
+ * host copy. */
 
 /* Eq. 9: end of the next migration, E = max(H, g * floor(max(0, C - T) / g)).
  * Requires H >= 0, C >= H, T >= 0, g >= 1 and H a multiple of g; returns -1

@@ -114,6 +114,10 @@ ss_status validate_desc(const ss_round_desc *d) {
     return fail(SS_ERR_INVALID_ARGUMENT, "split_tokens must be 0 or a positive multiple of %d", ss::kTile);
   if (d->mfma_min_rows < 0 || d->mfma_min_rows > ss::kMaxValuRows + 1)
     return fail(SS_ERR_INVALID_ARGUMENT, "mfma_min_rows must be in [0, %d]", ss::kMaxValuRows + 1);
+  if (d->counters_zeroed != 0 && d->counters_zeroed != 1)
+    return fail(SS_ERR_INVALID_ARGUMENT, "counters_zeroed must be 0 or 1");
+  if ((long)d->num_requests * d->num_kv_heads > (1L << 24))
+    return fail(SS_ERR_INVALID_ARGUMENT, "num_requests * num_kv_heads too large");
   if (d->kv_layout != SS_KV_TOKEN_MAJOR && d->kv_layout != SS_KV_HEAD_MAJOR && d->kv_layout != SS_KV_HEAD_MAJOR_KV)
     return fail(SS_ERR_INVALID_ARGUMENT, "kv_layout must be SS_KV_TOKEN_MAJOR, SS_KV_HEAD_MAJOR or SS_KV_HEAD_MAJOR_KV");
   const int G = d->num_q_heads / d->num_kv_heads;
@@ -134,12 +138,15 @@ ss_status validate_desc(const ss_round_desc *d) {
   return SS_OK;
 }
 
-// Workspace: slot states a, m, l, then the claim counters of the balanced
-// history launches.
-size_t workspace_bytes_rows(long R) {
+// Workspace: slot states a, m, l, then the counter block: kClaimCounters
+// words (the first is the balancing tail's claim counter), then one
+// finished-unit counter per (request, KV head) for fused finalize launches.
+long counter_words(long B, long Hkv) { return ss::kClaimCounters + B * Hkv; }
+
+size_t workspace_bytes_rows(long R, long B, long Hkv) {
   const size_t a = align_up((size_t)ss::kNumSlots * R * ss::kHeadDim * sizeof(float), 256);
   const size_t m = align_up((size_t)ss::kNumSlots * R * sizeof(float), 256);
-  return a + 2 * m + align_up(ss::kClaimCounters * sizeof(uint32_t), 256);
+  return a + 2 * m + align_up((size_t)counter_words(B, Hkv) * sizeof(uint32_t), 256);
 }
 
 }  // namespace
@@ -149,14 +156,19 @@ struct ss_round {
   float scale;
   int32_t max_chunk_tokens, split_tokens, mfma_min_rows, kv_layout, tail_permille;
   std::vector<int32_t> n_cand, row_off;
-  uint32_t *claims = nullptr;        // kClaimCounters counters in the workspace
-  int balanced_launches = 0;         // history launches with a tail so far (counter index)
+  uint32_t *counters = nullptr;      // the workspace's counter block: claim counter, then done[B][Hkv]
+  int32_t counter_n = 0;             // words in the block
+  bool counters_ready = false;       // the block is known to be zero (cleared, or the caller said so)
   std::vector<int32_t> slots_used;   // per request: state slots written so far this round
   const uint16_t *q;
   const uint16_t *kc = nullptr, *vc = nullptr;   // candidate K/V, attended by finalize
   ss::State st;
   bool cand_done = false;
   bool finalized = false;
+  // A call failed after part of its work was enqueued (a launch or an
+  // event record returned an error): the slots that work writes and the
+  // host's record of them may disagree, so every later call is refused.
+  bool failed = false;
 };
 
 struct ss_pipeline {
@@ -167,12 +179,16 @@ struct ss_pipeline {
   hipEvent_t freed[2];
   bool used[2];
   int next;
+  // An upload or the attention after it failed part-way: a slot's events
+  // no longer describe its contents, so every later call is refused.
+  bool failed = false;
 };
 
 namespace {
 
 ss_status check_round(const ss_round *r) {
   if (r == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "round handle is null");
+  if (r->failed) return fail(SS_ERR_BAD_STATE, "an earlier call of this round failed part-way; destroy the round");
   if (r->finalized) return fail(SS_ERR_BAD_STATE, "round already finalized");
   return SS_OK;
 }
@@ -234,6 +250,7 @@ struct Plan {
   std::vector<ss::Item> items;
   std::vector<uint32_t> unit_first{0};
   std::vector<uint8_t> kind;
+  std::vector<int32_t> req;           // request of each unit
   std::vector<uint32_t> wg_first;
   std::vector<int32_t> slots_after;   // per request: slots in use after this call
   size_t tail_first = 0, num_tail = 0;
@@ -307,6 +324,7 @@ bool build_plan(const ss_round *r, int nchunks, const int32_t *len, long W, long
     if (ranges == 0) return;
     plan->unit_first.push_back((uint32_t)plan->items.size());
     plan->kind.push_back((uint8_t)kind_of(r, ub));
+    plan->req.push_back(ub);
     ++slot[ub];
     ranges = 0;
   };
@@ -422,8 +440,7 @@ ss_status plan_chunks(const ss_round *r, int nchunks, const int32_t *len, const 
   // or table entries, else none.
   const int permille = r->tail_permille == 0 ? kDefaultTailPermille : r->tail_permille;
   const long min_share = r->tail_permille == 0 ? kTailMinShare : kTailMinShareExplicit;
-  if (permille > 0 && total / W >= min_share && r->balanced_launches < ss::kClaimCounters &&
-      fits_one_launch(*plan)) {
+  if (permille > 0 && total / W >= min_share && fits_one_launch(*plan)) {
     Plan t;
     for (long tmin = kTailMin; tmin <= kTailMax; tmin *= 2)
       if (build_plan(r, nchunks, len, W, pmax, permille, tmin, &t) && fits_one_launch(t)) {
@@ -454,6 +471,10 @@ ss::ChunkParams *base_params(const ss_round *r, int nchunks, const void *const *
   p.claim = nullptr;
   p.tail_first = 0;
   p.num_tail = 0;
+  p.done = nullptr;
+  p.fin_first = 0;
+  p.kc = p.vc = nullptr;
+  p.out = p.lse = nullptr;
   return &p;
 }
 
@@ -479,8 +500,8 @@ hipError_t launch_units(ss::ChunkParams *p, const Plan &plan, F launch) {
     const uint32_t n = plan.unit_first[uend] - i0;
     std::memcpy(p->items, plan.items.data() + i0, n * sizeof(ss::Item));
     for (uint32_t u = u0; u < uend; ++u)
-      p->units[u - u0] = (plan.unit_first[u] - i0) | ((plan.unit_first[u + 1] - plan.unit_first[u]) << 16) |
-                         ((uint32_t)plan.kind[u] << 24);
+      p->units[u - u0] = ss::pack_unit(plan.unit_first[u] - i0, plan.unit_first[u + 1] - plan.unit_first[u],
+                                       plan.kind[u], (uint32_t)plan.req[u]);
     for (size_t w = w0; w <= w1; ++w) p->wg_first[w - w0] = (uint16_t)(plan.wg_first[w] - u0);
     p->num_items = (int32_t)n;
     p->num_units = (int32_t)(uend - u0);
@@ -507,44 +528,276 @@ hipError_t launch_items(P *p, const std::vector<ss::Item> &items, F launch) {
   return hipSuccess;
 }
 
-ss_status enqueue_history(ss_round *r, int nchunks, const void *const *k, const void *const *v,
-                          const int32_t *len, const std::vector<long> &tot, hipStream_t stream) {
-  long total = 0;
-  for (long t : tot) total += t;
-  if (total == 0) return SS_OK;
-  Plan plan;
-  ss_status s = plan_chunks(r, nchunks, len, tot, &plan);
-  if (s != SS_OK) return s;
-  ss::ChunkParams *p = base_params(r, nchunks, k, v, tot);
-  hipError_t e;
-  if (plan.num_tail > 0) {
-    // the round's first balanced launch zeroes every claim counter; each
-    // balanced launch then uses a counter of its own
-    if (r->balanced_launches == 0 &&
-        (e = ss::launch_clear_claims(r->claims, ss::kClaimCounters, stream)) != hipSuccess)
-      return hip_fail(e, "claim counter clear launch");
-    p->claim = r->claims + r->balanced_launches;
+// Before the round's first launch that uses the workspace's counter block:
+// zero the block with a one-wave kernel unless it is known to be zero
+// (ss_round_desc.counters_zeroed).  Every launch leaves the counters it used
+// at zero, so one clear serves the whole round.
+ss_status ensure_counters(ss_round *r, hipStream_t stream) {
+  if (r->counters_ready) return SS_OK;
+  const hipError_t e = ss::launch_clear_counters(r->counters, r->counter_n, stream);
+  if (e != hipSuccess) {
+    r->failed = true;
+    return hip_fail(e, "counter clear launch");
   }
-  e = launch_units(p, plan, [&](const ss::ChunkParams &q) { return ss::launch_chunk(q, stream); });
-  if (e != hipSuccess) return hip_fail(e, "history chunk kernel launch");
-  if (plan.num_tail > 0) ++r->balanced_launches;
-  r->slots_used = plan.slots_after;   // the slots written by this call are valid from now on
+  r->counters_ready = true;
+  return SS_OK;
+}
+
+// A validated and planned history call, ready to enqueue.
+struct Prepared {
+  std::vector<long> tot;
+  long total = 0;
+  Plan plan;
+};
+
+// Validate a history call and plan its launches; enqueues nothing.
+ss_status prepare_history(const ss_round *r, int nchunks, const void *const *k, const void *const *v,
+                          const int32_t *len, Prepared *pr) {
+  ss_status s = check_history_args(r, nchunks, k, v, len, &pr->tot);
+  if (s != SS_OK) return s;
+  pr->total = 0;
+  for (long t : pr->tot) pr->total += t;
+  if (pr->total == 0) return SS_OK;
+  return plan_chunks(r, nchunks, len, pr->tot, &pr->plan);
+}
+
+// Enqueue a prepared call: the stream waits for wait_before, the launches
+// run, signal_after is recorded.  A HIP error after the first enqueued
+// operation marks the round failed (its slots_used would no longer match
+// what the device writes).
+ss_status enqueue_history(ss_round *r, int nchunks, const void *const *k, const void *const *v,
+                          const Prepared &pr, hipEvent_t wait_before, hipEvent_t signal_after, hipStream_t stream) {
+  hipError_t e;
+  if (wait_before != nullptr && (e = hipStreamWaitEvent(stream, wait_before, 0)) != hipSuccess)
+    return hip_fail(e, "hipStreamWaitEvent (history)");
+  if (pr.total > 0) {
+    const Plan &plan = pr.plan;
+    ss::ChunkParams *p = base_params(r, nchunks, k, v, pr.tot);
+    if (plan.num_tail > 0) {
+      ss_status s = ensure_counters(r, stream);
+      if (s != SS_OK) return s;
+      p->claim = r->counters;   // zero at launch; the launch's last claim leaves it zero
+    }
+    e = launch_units(p, plan, [&](const ss::ChunkParams &q) { return ss::launch_chunk(q, stream); });
+    if (e != hipSuccess) {
+      r->failed = true;
+      return hip_fail(e, "history chunk kernel launch");
+    }
+    r->slots_used = plan.slots_after;   // the slots written by this call are valid from now on
+  }
+  if (signal_after != nullptr && (e = hipEventRecord(signal_after, stream)) != hipSuccess) {
+    r->failed = true;
+    return hip_fail(e, "hipEventRecord (history)");
+  }
   return SS_OK;
 }
 
 ss_status attend_history(ss_round *r, int nchunks, const void *const *k, const void *const *v, const int32_t *len,
                          hipEvent_t wait_before, hipEvent_t signal_after, hipStream_t stream) {
-  std::vector<long> tot;
-  ss_status s = check_history_args(r, nchunks, k, v, len, &tot);
+  Prepared pr;
+  ss_status s = prepare_history(r, nchunks, k, v, len, &pr);
   if (s != SS_OK) return s;
+  return enqueue_history(r, nchunks, k, v, pr, wait_before, signal_after, stream);
+}
+
+// Finalize item of request b: the slots to merge and, for a fused launch,
+// the number of the request's units in the launch.
+ss::Item fin_item(const ss_round *r, int b, int slots, int units) {
+  ss::Item it{};
+  it.tok_begin = 0;
+  it.tok_count = slots;
+  it.q_row0 = r->row_off[b];
+  it.n_cand = (uint8_t)r->n_cand[b];
+  it.chunk = 0;
+  it.slot = (uint8_t)units;
+  it.flags = 0;
+  return it;
+}
+
+bool check_out(float *out, float *lse, ss_status *s) {
+  if (out == nullptr || !aligned(out, 16)) {
+    *s = fail(SS_ERR_INVALID_ARGUMENT, "out must be non-null and 16-byte aligned");
+    return false;
+  }
+  if (lse != nullptr && !aligned(lse, 4)) {
+    *s = fail(SS_ERR_INVALID_ARGUMENT, "lse must be 4-byte aligned");
+    return false;
+  }
+  return true;
+}
+
+// The finalize kernel: one workgroup per (KV head, request).
+ss_status enqueue_finalize(ss_round *r, float *out, float *lse, hipStream_t stream) {
+  static thread_local ss::FinalParams p;
+  p.kc = r->kc;
+  p.vc = r->vc;
+  p.q = r->q;
+  p.out = out;
+  p.lse = lse;
+  p.st = r->st;
+  p.Hq = r->Hq;
+  p.Hkv = r->Hkv;
+  p.G = r->G;
+  p.scale_log2 = r->scale * 1.4426950408889634f;
+  std::vector<ss::Item> items(r->B);
+  for (int b = 0; b < r->B; ++b) items[b] = fin_item(r, b, r->slots_used[b], 0);
+  const hipError_t e = launch_items(&p, items, [&](const ss::FinalParams &q) { return ss::launch_finalize(q, stream); });
+  if (e != hipSuccess) {
+    r->failed = true;
+    return hip_fail(e, "finalize kernel launch");
+  }
+  r->finalized = true;
+  return SS_OK;
+}
+
+// The plan of a history call whose launch also finalizes the round: every
+// request gets its finalize item (after the units' items), and a request
+// without tokens in the call gets a kUnitFinal unit, spread over the
+// workgroups' lists.  False if the result does not fit one launch.
+bool make_fused_plan(const ss_round *r, const Plan &plan, Plan *out, size_t *fin_first) {
+  if (r->B > ss::kMaxFusedRequests || !fits_one_launch(plan)) return false;
+  const size_t W = plan.wg_first.size() - 1;
+  std::vector<int> units(r->B, 0);
+  for (size_t u = 0; u < plan.units(); ++u) ++units[plan.req[u]];
+  std::vector<std::vector<int>> extra(W);
+  size_t k = 0;
+  for (int b = 0; b < r->B; ++b)
+    if (units[b] == 0) extra[k++ % W].push_back(b);
+  Plan q;
+  q.items = plan.items;
+  q.slots_after = plan.slots_after;
+  auto copy_unit = [&](size_t u) {
+    q.unit_first.push_back(plan.unit_first[u + 1] - plan.unit_first[u] + q.unit_first.back());
+    q.kind.push_back(plan.kind[u]);
+    q.req.push_back(plan.req[u]);
+  };
+  for (size_t w = 0; w < W; ++w) {
+    q.wg_first.push_back((uint32_t)q.units());
+    for (uint32_t u = plan.wg_first[w]; u < plan.wg_first[w + 1]; ++u) copy_unit(u);
+    for (int b : extra[w]) {
+      q.unit_first.push_back(q.unit_first.back());   // no items
+      q.kind.push_back((uint8_t)ss::kUnitFinal);
+      q.req.push_back(b);
+    }
+  }
+  q.wg_first.push_back((uint32_t)q.units());
+  q.tail_first = q.units();
+  for (size_t u = plan.tail_first; u < plan.units(); ++u) copy_unit(u);
+  q.num_tail = plan.num_tail;
+  *fin_first = q.items.size();
+  for (int b = 0; b < r->B; ++b) q.items.push_back(fin_item(r, b, q.slots_after[b], units[b] > 0 ? units[b] : 1));
+  if (q.units() > (size_t)ss::kMaxUnits || q.items.size() > (size_t)ss::kMaxItems) return false;
+  *out = std::move(q);
+  return true;
+}
+
+// The round's last history call with the finalize fused into its launch
+// (or, where the call does not fit one fused launch, the history launches
+// followed by the finalize kernel).
+ss_status enqueue_history_final(ss_round *r, int nchunks, const void *const *k, const void *const *v,
+                                const Prepared &pr, hipEvent_t wait_before, hipEvent_t signal_after, float *out,
+                                float *lse, hipStream_t stream) {
+  Plan plan;
+  size_t fin_first = 0;
+  if (pr.total == 0 || !make_fused_plan(r, pr.plan, &plan, &fin_first)) {
+    ss_status s = enqueue_history(r, nchunks, k, v, pr, wait_before, signal_after, stream);
+    if (s != SS_OK) return s;
+    return enqueue_finalize(r, out, lse, stream);
+  }
   hipError_t e;
   if (wait_before != nullptr && (e = hipStreamWaitEvent(stream, wait_before, 0)) != hipSuccess)
     return hip_fail(e, "hipStreamWaitEvent (history)");
-  s = enqueue_history(r, nchunks, k, v, len, tot, stream);
+  ss_status s = ensure_counters(r, stream);
   if (s != SS_OK) return s;
-  if (signal_after != nullptr && (e = hipEventRecord(signal_after, stream)) != hipSuccess)
+  ss::ChunkParams *p = base_params(r, nchunks, k, v, pr.tot);
+  const size_t W = plan.wg_first.size() - 1;
+  for (size_t u = 0; u < plan.units(); ++u)
+    p->units[u] = ss::pack_unit(plan.unit_first[u], plan.unit_first[u + 1] - plan.unit_first[u], plan.kind[u],
+                                (uint32_t)plan.req[u]);
+  for (size_t w = 0; w <= W; ++w) p->wg_first[w] = (uint16_t)plan.wg_first[w];
+  std::memcpy(p->items, plan.items.data(), plan.items.size() * sizeof(ss::Item));
+  p->num_items = (int32_t)plan.items.size();
+  p->num_units = (int32_t)plan.units();
+  p->num_wgs = (int32_t)W;
+  p->tail_first = plan.num_tail > 0 ? (int32_t)plan.tail_first : 0;
+  p->num_tail = (int32_t)plan.num_tail;
+  p->claim = r->counters;
+  p->done = r->counters + ss::kClaimCounters;
+  p->fin_first = (int32_t)fin_first;
+  p->kc = r->kc;
+  p->vc = r->vc;
+  p->out = out;
+  p->lse = lse;
+  e = ss::launch_chunk(*p, stream);
+  if (e != hipSuccess) {
+    r->failed = true;
+    return hip_fail(e, "history chunk kernel launch (fused finalize)");
+  }
+  r->slots_used = plan.slots_after;
+  r->finalized = true;
+  if (signal_after != nullptr && (e = hipEventRecord(signal_after, stream)) != hipSuccess) {
+    r->failed = true;
     return hip_fail(e, "hipEventRecord (history)");
+  }
   return SS_OK;
+}
+
+// Pointer checks of a host<->device copy: the host side must be pinned
+// (page-locked) memory, the device side device memory.
+ss_status check_copy(const void *dst, const void *src, size_t bytes, hipMemcpyKind kind) {
+  const bool h2d = kind == hipMemcpyHostToDevice;
+  const void *host = h2d ? src : dst;
+  const void *dev = h2d ? dst : src;
+  if (dst == nullptr || src == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "copy pointers must be non-null");
+  if (bytes == 0) return fail(SS_ERR_INVALID_ARGUMENT, "copy of 0 bytes");
+  hipPointerAttribute_t attr;
+  std::memset(&attr, 0, sizeof attr);
+  hipError_t e = hipPointerGetAttributes(&attr, host);
+  if (e != hipSuccess || attr.type != hipMemoryTypeHost) {
+    (void)hipGetLastError();
+    return fail(SS_ERR_NOT_PINNED, "%s %p is not pinned host memory", h2d ? "upload source" : "download destination",
+                host);
+  }
+  std::memset(&attr, 0, sizeof attr);
+  e = hipPointerGetAttributes(&attr, dev);
+  if (e != hipSuccess || attr.type != hipMemoryTypeDevice) {
+    (void)hipGetLastError();
+    return fail(SS_ERR_INVALID_ARGUMENT, "%s %p is not device memory", h2d ? "upload destination" : "download source",
+                dev);
+  }
+  return SS_OK;
+}
+
+// Enqueue a checked copy on copy_stream: wait for wait_before, copy, record
+// signal_after.  *enqueued (nullable) tells whether any of it reached the
+// stream before an error.
+ss_status enqueue_copy(void *dst, const void *src, size_t bytes, hipMemcpyKind kind, hipStream_t copy_stream,
+                       hipEvent_t wait_before, hipEvent_t signal_after, bool *enqueued) {
+  if (enqueued != nullptr) *enqueued = false;
+  hipError_t e;
+  if (wait_before != nullptr && (e = hipStreamWaitEvent(copy_stream, wait_before, 0)) != hipSuccess)
+    return hip_fail(e, "hipStreamWaitEvent (copy)");
+  if (enqueued != nullptr) *enqueued = wait_before != nullptr;
+  if ((e = hipMemcpyAsync(dst, src, bytes, kind, copy_stream)) != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  if (enqueued != nullptr) *enqueued = true;
+  if (signal_after != nullptr && (e = hipEventRecord(signal_after, copy_stream)) != hipSuccess)
+    return hip_fail(e, "hipEventRecord (copy)");
+  return SS_OK;
+}
+
+// Run an entry point's body with C++ exceptions turned into statuses: host
+// allocation failures (std::vector, new) become SS_ERR_OUT_OF_MEMORY and
+// nothing escapes the C ABI.  Every body allocates before it enqueues
+// anything, so such a failure leaves the device work untouched.
+template <typename F>
+ss_status guarded(F body) {
+  try {
+    return body();
+  } catch (const std::bad_alloc &) {
+    return fail(SS_ERR_OUT_OF_MEMORY, "out of host memory");
+  } catch (...) {
+    return fail(SS_ERR_INVALID_ARGUMENT, "unexpected C++ exception in the library");
+  }
 }
 
 }  // namespace
@@ -555,11 +808,18 @@ size_t ss_round_workspace_bytes(const ss_round_desc *desc) {
   if (validate_desc(desc) != SS_OK) return 0;
   long R = 0;
   for (int b = 0; b < desc->num_requests; ++b) R += (long)desc->num_cand[b] * desc->num_q_heads;
-  return workspace_bytes_rows(R);
+  return workspace_bytes_rows(R, desc->num_requests, desc->num_kv_heads);
 }
 
-ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q, void *workspace,
-                        size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The common part of the round-init entry points: validate, lay out the
+// workspace (slot states a, m, l, then the claim counters) and create the
+// host handle.
+ss_status init_round(ss_round **out, const ss_round_desc *desc, const void *q, void *workspace,
+                     size_t workspace_bytes) {
   if (out == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "out is null");
   *out = nullptr;
   ss_status s = validate_desc(desc);
@@ -567,14 +827,14 @@ ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q
   if (q == nullptr || !aligned(q, 16)) return fail(SS_ERR_INVALID_ARGUMENT, "q must be non-null and 16-byte aligned");
   long R = 0;
   for (int b = 0; b < desc->num_requests; ++b) R += (long)desc->num_cand[b] * desc->num_q_heads;
-  const size_t need = workspace_bytes_rows(R);
+  const size_t need = workspace_bytes_rows(R, desc->num_requests, desc->num_kv_heads);
   if (workspace == nullptr || !aligned(workspace, 256))
     return fail(SS_ERR_WORKSPACE, "workspace must be non-null and 256-byte aligned");
   if (workspace_bytes < need)
     return fail(SS_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
 
   ss_round *r = new (std::nothrow) ss_round();
-  if (r == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "out of host memory");
+  if (r == nullptr) return fail(SS_ERR_OUT_OF_MEMORY, "out of host memory");
   r->B = desc->num_requests;
   r->Hq = desc->num_q_heads;
   r->Hkv = desc->num_kv_heads;
@@ -583,8 +843,14 @@ ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q
   r->max_chunk_tokens = desc->max_chunk_tokens;
   r->split_tokens = desc->split_tokens;
   r->mfma_min_rows = desc->mfma_min_rows;
-  r->n_cand.assign(desc->num_cand, desc->num_cand + desc->num_requests);
-  r->row_off.resize(r->B);
+  try {
+    r->n_cand.assign(desc->num_cand, desc->num_cand + desc->num_requests);
+    r->row_off.resize(r->B);
+    r->slots_used.assign(r->B, 0);   // every slot starts empty: nothing to enqueue
+  } catch (const std::bad_alloc &) {
+    delete r;
+    return fail(SS_ERR_OUT_OF_MEMORY, "out of host memory");
+  }
   int32_t acc = 0;
   for (int b = 0; b < r->B; ++b) {
     r->row_off[b] = acc;
@@ -597,54 +863,45 @@ ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q
   r->st.a = reinterpret_cast<float *>(ws);
   r->st.m = reinterpret_cast<float *>(ws + a_bytes);
   r->st.l = reinterpret_cast<float *>(ws + a_bytes + m_bytes);
-  r->claims = reinterpret_cast<uint32_t *>(ws + a_bytes + 2 * m_bytes);
+  r->counters = reinterpret_cast<uint32_t *>(ws + a_bytes + 2 * m_bytes);
+  r->counter_n = (int32_t)counter_words(r->B, r->Hkv);
+  r->counters_ready = desc->counters_zeroed != 0;
   r->tail_permille = desc->balance_permille;
   r->st.R = (int32_t)R;
   r->kv_layout = desc->kv_layout;
-  r->slots_used.assign(r->B, 0);   // every slot starts empty: nothing to enqueue
-  (void)stream;
   *out = r;
   return SS_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+  (void)stream;   // the empty state is tracked on the host: nothing to enqueue
+  return init_round(out, desc, q, workspace, workspace_bytes);
+}
+
 ss_status ss_upload_chunk(void *dst_device, const void *src_pinned_host, size_t bytes, hipStream_t copy_stream,
                           hipEvent_t wait_before, hipEvent_t signal_after) {
-  if (dst_device == nullptr || src_pinned_host == nullptr)
-    return fail(SS_ERR_INVALID_ARGUMENT, "upload pointers must be non-null");
-  if (bytes == 0) return fail(SS_ERR_INVALID_ARGUMENT, "upload of 0 bytes");
-  hipPointerAttribute_t attr;
-  std::memset(&attr, 0, sizeof attr);
-  hipError_t e = hipPointerGetAttributes(&attr, src_pinned_host);
-  if (e != hipSuccess || attr.type != hipMemoryTypeHost) {
-    (void)hipGetLastError();
-    return fail(SS_ERR_NOT_PINNED, "upload source %p is not pinned host memory", src_pinned_host);
-  }
-  std::memset(&attr, 0, sizeof attr);
-  e = hipPointerGetAttributes(&attr, dst_device);
-  if (e != hipSuccess || attr.type != hipMemoryTypeDevice) {
-    (void)hipGetLastError();
-    return fail(SS_ERR_INVALID_ARGUMENT, "upload destination %p is not device memory", dst_device);
-  }
-  if (wait_before != nullptr && (e = hipStreamWaitEvent(copy_stream, wait_before, 0)) != hipSuccess)
-    return hip_fail(e, "hipStreamWaitEvent (upload)");
-  if ((e = hipMemcpyAsync(dst_device, src_pinned_host, bytes, hipMemcpyHostToDevice, copy_stream)) != hipSuccess)
-    return hip_fail(e, "hipMemcpyAsync (upload)");
-  if (signal_after != nullptr && (e = hipEventRecord(signal_after, copy_stream)) != hipSuccess)
-    return hip_fail(e, "hipEventRecord (upload)");
-  return SS_OK;
+  ss_status s = check_copy(dst_device, src_pinned_host, bytes, hipMemcpyHostToDevice);
+  if (s != SS_OK) return s;
+  return enqueue_copy(dst_device, src_pinned_host, bytes, hipMemcpyHostToDevice, copy_stream, wait_before,
+                      signal_after, nullptr);
 }
 
 ss_status ss_attend_history_chunk(ss_round *r, const void *k, const void *v, const int32_t *len,
                                   hipEvent_t wait_before, hipEvent_t signal_after, hipStream_t stream) {
   const void *kk[1] = {k};
   const void *vv[1] = {v};
-  return attend_history(r, 1, kk, vv, len, wait_before, signal_after, stream);
+  return guarded([&] { return attend_history(r, 1, kk, vv, len, wait_before, signal_after, stream); });
 }
 
 ss_status ss_attend_history_chunks(ss_round *r, int32_t num_chunks, const void *const *k, const void *const *v,
                                    const int32_t *len, hipEvent_t wait_before, hipEvent_t signal_after,
                                    hipStream_t stream) {
-  return attend_history(r, num_chunks, k, v, len, wait_before, signal_after, stream);
+  return guarded([&] { return attend_history(r, num_chunks, k, v, len, wait_before, signal_after, stream); });
 }
 
 ss_status ss_attend_local_candidates(ss_round *r, const void *k_cand, const void *v_cand, hipStream_t stream) {
@@ -663,34 +920,28 @@ ss_status ss_attend_local_candidates(ss_round *r, const void *k_cand, const void
 }
 
 ss_status ss_round_finalize(ss_round *r, float *out, float *lse, hipStream_t stream) {
-  ss_status s = check_round(r);
-  if (s != SS_OK) return s;
-  if (!r->cand_done) return fail(SS_ERR_BAD_STATE, "finalize before ss_attend_local_candidates");
-  if (out == nullptr || !aligned(out, 16)) return fail(SS_ERR_INVALID_ARGUMENT, "out must be non-null and 16-byte aligned");
-  if (lse != nullptr && !aligned(lse, 4)) return fail(SS_ERR_INVALID_ARGUMENT, "lse must be 4-byte aligned");
-  static thread_local ss::FinalParams p;
-  p.kc = r->kc;
-  p.vc = r->vc;
-  p.q = r->q;
-  p.out = out;
-  p.lse = lse;
-  p.st = r->st;
-  p.Hq = r->Hq;
-  p.Hkv = r->Hkv;
-  p.G = r->G;
-  p.scale_log2 = r->scale * 1.4426950408889634f;
-  std::vector<ss::Item> items(r->B);
-  for (int b = 0; b < r->B; ++b) {
-    items[b].tok_begin = 0;
-    items[b].tok_count = r->slots_used[b];
-    items[b].q_row0 = r->row_off[b];
-    items[b].n_cand = (int16_t)r->n_cand[b];
-    items[b].slot = 0;
-  }
-  const hipError_t e = launch_items(&p, items, [&](const ss::FinalParams &q) { return ss::launch_finalize(q, stream); });
-  if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
-  r->finalized = true;
-  return SS_OK;
+  return guarded([&]() -> ss_status {
+    ss_status s = check_round(r);
+    if (s != SS_OK) return s;
+    if (!r->cand_done) return fail(SS_ERR_BAD_STATE, "finalize before ss_attend_local_candidates");
+    if (!check_out(out, lse, &s)) return s;
+    return enqueue_finalize(r, out, lse, stream);
+  });
+}
+
+ss_status ss_round_finalize_chunks(ss_round *r, int32_t num_chunks, const void *const *k, const void *const *v,
+                                   const int32_t *len, hipEvent_t wait_before, hipEvent_t signal_after, float *out,
+                                   float *lse, hipStream_t stream) {
+  return guarded([&]() -> ss_status {
+    ss_status s = check_round(r);
+    if (s != SS_OK) return s;
+    if (!r->cand_done) return fail(SS_ERR_BAD_STATE, "finalize before ss_attend_local_candidates");
+    if (!check_out(out, lse, &s)) return s;
+    Prepared pr;
+    s = prepare_history(r, num_chunks, k, v, len, &pr);
+    if (s != SS_OK) return s;
+    return enqueue_history_final(r, num_chunks, k, v, pr, wait_before, signal_after, out, lse, stream);
+  });
 }
 
 void ss_round_destroy(ss_round *r) { delete r; }
@@ -703,7 +954,7 @@ ss_status ss_pipeline_create(ss_pipeline **out, void *staging0, void *staging1, 
     return fail(SS_ERR_INVALID_ARGUMENT, "staging slots must be non-null and 256-byte aligned");
   if (slot_bytes == 0) return fail(SS_ERR_INVALID_ARGUMENT, "slot_bytes must be > 0");
   ss_pipeline *p = new (std::nothrow) ss_pipeline();
-  if (p == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "out of host memory");
+  if (p == nullptr) return fail(SS_ERR_OUT_OF_MEMORY, "out of host memory");
   p->slot[0] = static_cast<char *>(staging0);
   p->slot[1] = static_cast<char *>(staging1);
   p->slot_bytes = slot_bytes;
@@ -728,7 +979,9 @@ ss_status ss_pipeline_create(ss_pipeline **out, void *staging0, void *staging1, 
 
 ss_status ss_pipeline_attend_chunks(ss_pipeline *p, ss_round *r, int32_t num_chunks, const void *host_kv,
                                     const int32_t *len, hipStream_t stream) {
+  return guarded([&]() -> ss_status {
   if (p == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "pipeline is null");
+  if (p->failed) return fail(SS_ERR_BAD_STATE, "an earlier call of this pipeline failed part-way; destroy it");
   ss_status s = check_round(r);
   if (s != SS_OK) return s;
   if (num_chunks < 1 || num_chunks > ss::kMaxChunks)
@@ -747,20 +1000,37 @@ ss_status ss_pipeline_attend_chunks(ss_pipeline *p, ss_round *r, int32_t num_chu
     vv[c] = p->slot[sl] + bytes + (r->kv_layout == SS_KV_HEAD_MAJOR_KV ? ss::kHeadDim * 2 : half);
     bytes += 2 * half;
   }
-  std::vector<long> tot;
-  s = check_history_args(r, num_chunks, kk.data(), vv.data(), len, &tot);
+  // everything that can be refused is checked (and the launches planned)
+  // before the upload is enqueued
+  Prepared pr;
+  s = prepare_history(r, num_chunks, kk.data(), vv.data(), len, &pr);
   if (s != SS_OK) return s;
   if (bytes == 0) return SS_OK;
   if (host_kv == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "host_kv is null");
   if (bytes > p->slot_bytes)
     return fail(SS_ERR_INVALID_ARGUMENT, "chunks need %zu bytes > slot_bytes %zu", bytes, p->slot_bytes);
-  s = ss_upload_chunk(p->slot[sl], host_kv, bytes, p->copy, p->used[sl] ? p->freed[sl] : nullptr, p->ready[sl]);
+  s = check_copy(p->slot[sl], host_kv, bytes, hipMemcpyHostToDevice);
   if (s != SS_OK) return s;
-  s = attend_history(r, num_chunks, kk.data(), vv.data(), len, p->ready[sl], p->freed[sl], stream);
-  if (s != SS_OK) return s;
+  bool enqueued = false;
+  s = enqueue_copy(p->slot[sl], host_kv, bytes, hipMemcpyHostToDevice, p->copy, p->used[sl] ? p->freed[sl] : nullptr,
+                   p->ready[sl], &enqueued);
+  if (s != SS_OK) {
+    // a wait or copy already on the copy stream leaves the slot's events
+    // out of step with its contents
+    if (enqueued) p->failed = true;
+    return s;
+  }
+  s = enqueue_history(r, num_chunks, kk.data(), vv.data(), pr, p->ready[sl], p->freed[sl], stream);
+  if (s != SS_OK) {
+    // the upload is in flight and the slot's free event may never be
+    // recorded after its readers
+    p->failed = true;
+    return s;
+  }
   p->used[sl] = true;
   p->next = sl ^ 1;
   return SS_OK;
+  });
 }
 
 ss_status ss_pipeline_attend_chunk(ss_pipeline *p, ss_round *r, const void *host_kv, const int32_t *len,
@@ -797,6 +1067,7 @@ const char *ss_status_string(ss_status s) {
     case SS_ERR_NOT_PINNED: return "SS_ERR_NOT_PINNED";
     case SS_ERR_WORKSPACE: return "SS_ERR_WORKSPACE";
     case SS_ERR_HIP: return "SS_ERR_HIP";
+    case SS_ERR_OUT_OF_MEMORY: return "SS_ERR_OUT_OF_MEMORY";
     default: return "SS_ERR_UNKNOWN";
   }
 }

@@ -20,7 +20,7 @@ class RoundBuffers:
 
     def __init__(self, w: Workload, layer: int = 0, device="cuda", split_tokens: int = 0,
                  mfma_min_rows: int = 0, max_chunk_tokens: Optional[int] = None,
-                 kv_layout: int = ss.SS_KV_TOKEN_MAJOR, balance_permille: int = 0):
+                 kv_layout: int = ss.SS_KV_TOKEN_MAJOR, balance_permille: int = 0, counters_zeroed: int = 0):
         self.w = w
         self.layer = layer
         self.device = device
@@ -30,11 +30,13 @@ class RoundBuffers:
         mct = max_chunk_tokens or max(1, max(sum(w.chunk_lens(j)) for j in range(max(1, w.num_chunks))))
         self.kv_layout = kv_layout
         self.desc = ss.make_desc(w.num_cand, w.num_q_heads, w.num_kv_heads, w.head_dim, w.softmax_scale,
-                                 mct, split_tokens, mfma_min_rows, kv_layout, balance_permille)
+                                 mct, split_tokens, mfma_min_rows, kv_layout, balance_permille, counters_zeroed)
         self.ws_bytes = ss.ss_round_workspace_bytes(self.desc)
         if self.ws_bytes == 0:
             raise ss.SpecStreamError(ss.SS_ERR_INVALID_ARGUMENT, "ss_round_workspace_bytes", ss.ss_last_error())
-        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        # with counters_zeroed the rounds rely on the workspace's counter block being zero: zero-fill it once
+        alloc = torch.zeros if counters_zeroed else torch.empty
+        self.ws = alloc(self.ws_bytes, dtype=torch.uint8, device=device)
         rows = w.total_rows
         self.out = torch.empty(rows, w.num_q_heads, w.head_dim, dtype=torch.float32, device=device)
         self.lse = torch.empty(rows, w.num_q_heads, dtype=torch.float32, device=device)
@@ -55,35 +57,41 @@ def hbm_history(w: Workload, layer: int = 0, device="cuda", kv_layout: int = ss.
 
 def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor]], stream: int,
               order: Optional[Sequence[int]] = None, cand_position: Optional[int] = None,
-              lens: Optional[Sequence[Sequence[int]]] = None, batch: int = 1) -> None:
+              lens: Optional[Sequence[Sequence[int]]] = None, batch: int = 1, fused: bool = False) -> None:
     """Enqueue one whole round (init, history chunks, candidates, finalize)
     on `stream`; results land in b.out / b.lse.  ``batch`` > 1 groups that
-    many consecutive chunks into one ss_attend_history_chunks call."""
+    many consecutive chunks into one ss_attend_history_chunks call.  With
+    ``fused`` the last group of chunks and the finalize go through one
+    ss_round_finalize_chunks call (the candidates are attended before it)."""
     w = b.w
     order = list(range(len(chunks))) if order is None else list(order)
     pos = len(order) if cand_position is None else cand_position
+    step = max(1, batch)
+    groups = [order[i0:i0 + step] for i0 in range(0, len(order), step)]
+    if fused and groups:
+        pos = min(pos, (len(groups) - 1) * step)   # candidates before the fused last call
     r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream)
-    if batch > 1:
-        try:
-            for i0 in range(0, len(order), batch):
-                grp = order[i0:i0 + batch]
-                ks = [chunks[j][0].data_ptr() if chunks[j][0].numel() else 0 for j in grp]
-                vs = [chunks[j][1].data_ptr() if chunks[j][1].numel() else 0 for j in grp]
-                ls = [w.chunk_lens(j) if lens is None else lens[j] for j in grp]
-                ss.ss_attend_history_chunks(r, ks, vs, ls, None, None, stream)
-            ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
-            ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream)
-        finally:
-            ss.ss_round_destroy(r)
-        return
+
+    def args(grp):
+        ks = [chunks[j][0].data_ptr() if chunks[j][0].numel() else 0 for j in grp]
+        vs = [chunks[j][1].data_ptr() if chunks[j][1].numel() else 0 for j in grp]
+        ls = [w.chunk_lens(j) if lens is None else lens[j] for j in grp]
+        return ks, vs, ls
+
     try:
-        for idx, j in enumerate(order):
-            if idx == pos:
+        done = 0
+        for gi, grp in enumerate(groups):
+            if done <= pos < done + len(grp) or (pos == done and gi == 0):
                 ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
-            k, v = chunks[j]
-            ln = w.chunk_lens(j) if lens is None else lens[j]
-            ss.ss_attend_history_chunk(r, k.data_ptr() if k.numel() else 0, v.data_ptr() if v.numel() else 0,
-                                       ln, None, None, stream)
+            ks, vs, ls = args(grp)
+            if fused and gi == len(groups) - 1:
+                ss.ss_round_finalize_chunks(r, ks, vs, ls, b.out.data_ptr(), b.lse.data_ptr(), None, None, stream)
+                return
+            if batch > 1:
+                ss.ss_attend_history_chunks(r, ks, vs, ls, None, None, stream)
+            else:
+                ss.ss_attend_history_chunk(r, ks[0], vs[0], ls[0], None, None, stream)
+            done += len(grp)
         if pos >= len(order):
             ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
         ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream)
@@ -92,7 +100,7 @@ def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor
 
 
 def capture_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor]], batch: int = 1,
-                  pool=None) -> "torch.cuda.CUDAGraph":
+                  pool=None, fused: bool = False) -> "torch.cuda.CUDAGraph":
     """Capture one whole round (the same calls as run_round) into a HIP graph.
 
     Every step the library enqueues is a kernel launch with its arguments by
@@ -104,7 +112,7 @@ def capture_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Te
     g = torch.cuda.CUDAGraph()
     torch.cuda.synchronize()
     with torch.cuda.graph(g, pool=pool):
-        run_round(b, chunks, torch.cuda.current_stream().cuda_stream, batch=batch)
+        run_round(b, chunks, torch.cuda.current_stream().cuda_stream, batch=batch, fused=fused)
     return g
 
 
@@ -192,3 +200,67 @@ def run_round_streamed(b: RoundBuffers, host: HostHistory, pipe: Pipeline, strea
         ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream)
     finally:
         ss.ss_round_destroy(r)
+
+
+def _chunk_vofs(w: Workload, host: HostHistory, j: int, kv_layout: int) -> int:
+    """Bytes from a chunk's K to its V in a staging buffer holding the chunk."""
+    return 2 * w.head_dim if kv_layout == ss.SS_KV_HEAD_MAJOR_KV else host.sizes[j] // 2
+
+
+def run_round_restored(b: RoundBuffers, host: HostHistory, dev: Sequence[torch.Tensor], copy: "torch.cuda.Stream",
+                       stream: int) -> None:
+    """Restore, then attend: every chunk of the history goes to its own
+    device buffer (``dev[j]``, at least host.sizes[j] bytes) on the copy
+    stream, and one batched call, fused with finalize, attends all of them
+    once the last upload is done."""
+    w = b.w
+    n = w.num_chunks
+    done = ss.ss_event_create()
+    try:
+        last = max([j for j in range(n) if host.sizes[j]], default=-1)
+        for j in range(n):
+            if host.sizes[j]:
+                ss.ss_upload_chunk(dev[j].data_ptr(), host.chunk_ptr(j), host.sizes[j], copy.cuda_stream, None,
+                                   done if j == last else None)
+        r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream)
+        try:
+            ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
+            ks = [dev[j].data_ptr() for j in range(n)]
+            vs = [dev[j].data_ptr() + _chunk_vofs(w, host, j, b.kv_layout) for j in range(n)]
+            ss.ss_round_finalize_chunks(r, ks, vs, [w.chunk_lens(j) for j in range(n)], b.out.data_ptr(),
+                                        b.lse.data_ptr(), done if last >= 0 else None, None, stream)
+        finally:
+            ss.ss_round_destroy(r)
+    finally:
+        torch.cuda.synchronize()      # the events are destroyed only after the work that uses them
+        ss.ss_event_destroy(done)
+
+
+def run_round_single_slot(b: RoundBuffers, host: HostHistory, slot: torch.Tensor, copy: "torch.cuda.Stream",
+                          stream: int) -> None:
+    """Chunk by chunk through one staging buffer: chunk j is uploaded into
+    ``slot`` once chunk j-1's attention has read it (its free event), and
+    attended once its upload is done (its ready event), so uploads and
+    attention alternate without overlapping."""
+    w = b.w
+    ready, free = ss.ss_event_create(), ss.ss_event_create()
+    try:
+        r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream)
+        try:
+            used = False
+            for j in range(w.num_chunks):
+                if not host.sizes[j]:
+                    continue
+                ss.ss_upload_chunk(slot.data_ptr(), host.chunk_ptr(j), host.sizes[j], copy.cuda_stream,
+                                   free if used else None, ready)
+                ss.ss_attend_history_chunk(r, slot.data_ptr(), slot.data_ptr() + _chunk_vofs(w, host, j, b.kv_layout),
+                                           w.chunk_lens(j), ready, free, stream)
+                used = True
+            ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
+            ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream)
+        finally:
+            ss.ss_round_destroy(r)
+    finally:
+        torch.cuda.synchronize()
+        ss.ss_event_destroy(ready)
+        ss.ss_event_destroy(free)

@@ -23,6 +23,7 @@ SS_ERR_BAD_STATE = -3
 SS_ERR_NOT_PINNED = -4
 SS_ERR_WORKSPACE = -5
 SS_ERR_HIP = -6
+SS_ERR_OUT_OF_MEMORY = -7
 
 SS_KV_TOKEN_MAJOR = 0   # history chunk [sum len][Hkv][d]
 SS_KV_HEAD_MAJOR = 1    # history chunk [Hkv][sum len][d]
@@ -31,7 +32,8 @@ SS_KV_HEAD_MAJOR_KV = 2  # history chunk [Hkv][sum len][2][d]: K and V rows of a
 EXPORTED = (
     "ss_round_workspace_bytes", "ss_round_init", "ss_upload_chunk", "ss_attend_history_chunk",
     "ss_attend_history_chunks",
-    "ss_attend_local_candidates", "ss_round_finalize", "ss_round_destroy", "ss_pipeline_create",
+    "ss_attend_local_candidates", "ss_round_finalize", "ss_round_finalize_chunks",
+    "ss_round_destroy", "ss_pipeline_create",
     "ss_pipeline_attend_chunk", "ss_pipeline_attend_chunks", "ss_pipeline_destroy", "ss_event_create", "ss_event_destroy",
     "ss_status_string", "ss_last_error",
     "ss_tier_endpoint", "ss_tier_create", "ss_tier_destroy", "ss_tier_get", "ss_tier_extend", "ss_tier_commit",
@@ -59,19 +61,20 @@ class ss_round_desc(ctypes.Structure):
         ("mfma_min_rows", ctypes.c_int32),
         ("kv_layout", ctypes.c_int32),
         ("balance_permille", ctypes.c_int32),
+        ("counters_zeroed", ctypes.c_int32),
     ]
 
 
 def make_desc(num_cand: Sequence[int], num_q_heads: int, num_kv_heads: int, head_dim: int = 128,
               softmax_scale: Optional[float] = None, max_chunk_tokens: int = 1 << 30,
               split_tokens: int = 0, mfma_min_rows: int = 0, kv_layout: int = SS_KV_TOKEN_MAJOR,
-              balance_permille: int = 0) -> ss_round_desc:
+              balance_permille: int = 0, counters_zeroed: int = 0) -> ss_round_desc:
     """Build a descriptor; the candidate-count array is kept alive on it."""
     arr = (ctypes.c_int32 * len(num_cand))(*[int(x) for x in num_cand])
     d = ss_round_desc(len(num_cand), num_q_heads, num_kv_heads, head_dim,
                       (head_dim ** -0.5) if softmax_scale is None else softmax_scale,
                       ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)), max_chunk_tokens, split_tokens,
-                      mfma_min_rows, kv_layout, balance_permille)
+                      mfma_min_rows, kv_layout, balance_permille, counters_zeroed)
     d._keep = arr
     return d
 
@@ -100,6 +103,7 @@ def load() -> ctypes.CDLL:
         "ss_attend_history_chunks": (I32, [P, I32, ctypes.POINTER(P), ctypes.POINTER(P), PI32, P, P, P]),
         "ss_attend_local_candidates": (I32, [P, P, P, P]),
         "ss_round_finalize": (I32, [P, P, P, P]),
+        "ss_round_finalize_chunks": (I32, [P, I32, ctypes.POINTER(P), ctypes.POINTER(P), PI32, P, P, P, P, P]),
         "ss_round_destroy": (None, [P]),
         "ss_pipeline_create": (I32, [ctypes.POINTER(P), P, P, SZ, P]),
         "ss_pipeline_attend_chunk": (I32, [P, P, P, PI32, P]),
@@ -192,6 +196,17 @@ def ss_attend_local_candidates(r: int, k_cand: int, v_cand: int, stream: int = 0
 
 def ss_round_finalize(r: int, out: int, lse: Optional[int] = None, stream: int = 0) -> None:
     _check(load().ss_round_finalize(r, out, lse, stream), "ss_round_finalize")
+
+
+def ss_round_finalize_chunks(r: int, k: Sequence[int], v: Sequence[int], lens: Sequence[Sequence[int]],
+                             out: int, lse: Optional[int] = None, wait_before: Optional[int] = None,
+                             signal_after: Optional[int] = None, stream: int = 0) -> None:
+    n = len(k)
+    kp = (ctypes.c_void_p * n)(*k)
+    vp = (ctypes.c_void_p * n)(*v)
+    flat = [int(x) for row in lens for x in row]
+    _check(load().ss_round_finalize_chunks(r, n, kp, vp, (ctypes.c_int32 * len(flat))(*flat), wait_before,
+                                           signal_after, out, lse, stream), "ss_round_finalize_chunks")
 
 
 def ss_round_destroy(r: Optional[int]) -> None:

@@ -54,22 +54,25 @@ def test_status_strings(lib):
     for code, name in [(ss.SS_OK, "SS_OK"), (ss.SS_ERR_INVALID_ARGUMENT, "SS_ERR_INVALID_ARGUMENT"),
                        (ss.SS_ERR_UNSUPPORTED, "SS_ERR_UNSUPPORTED"), (ss.SS_ERR_BAD_STATE, "SS_ERR_BAD_STATE"),
                        (ss.SS_ERR_NOT_PINNED, "SS_ERR_NOT_PINNED"), (ss.SS_ERR_WORKSPACE, "SS_ERR_WORKSPACE"),
-                       (ss.SS_ERR_HIP, "SS_ERR_HIP")]:
+                       (ss.SS_ERR_HIP, "SS_ERR_HIP"), (ss.SS_ERR_OUT_OF_MEMORY, "SS_ERR_OUT_OF_MEMORY")]:
         assert ss.ss_status_string(code) == name
 
 
-def _ws(cands, hq):
+def _ws(cands, hq, hkv):
     rows = sum(cands) * hq
     a = -(-32 * rows * 128 * 4 // 256) * 256     # 32 state slots per row
     m = -(-32 * rows * 4 // 256) * 256
-    return a + 2 * m + 256          # + the claim counters of the balanced history calls
+    counters = -(-(64 + len(cands) * hkv) * 4 // 256) * 256   # claim words, then one per (request, KV head)
+    return a + 2 * m + counters
 
 
 def test_workspace_bytes_and_descriptor_validation(lib):
     d = ss.make_desc([6] * 16, 32, 8)
-    assert ss.ss_round_workspace_bytes(d) == _ws([6] * 16, 32)
+    assert ss.ss_round_workspace_bytes(d) == _ws([6] * 16, 32, 8)
     d = ss.make_desc([1, 8, 3], 8, 2)
-    assert ss.ss_round_workspace_bytes(d) == _ws([1, 8, 3], 8)
+    assert ss.ss_round_workspace_bytes(d) == _ws([1, 8, 3], 8, 2)
+    d = ss.make_desc([2] * 100, 8, 8)
+    assert ss.ss_round_workspace_bytes(d) == _ws([2] * 100, 8, 8)
     bad = [
         (ss.make_desc([5], 32, 6), "multiple"),                          # Hq % Hkv
         (ss.make_desc([5], 8, 2, head_dim=64), "head_dim"),
@@ -83,6 +86,7 @@ def test_workspace_bytes_and_descriptor_validation(lib):
         (ss.make_desc([4], 8, 2, kv_layout=3), "kv_layout"),
         (ss.make_desc([4], 8, 2, max_chunk_tokens=0), "max_chunk_tokens"),
         (ss.make_desc([4], 8, 2, balance_permille=501), "balance_permille"),
+        (ss.make_desc([4], 8, 2, counters_zeroed=2), "counters_zeroed"),
     ]
     for desc, word in bad:
         assert ss.ss_round_workspace_bytes(desc) == 0
@@ -125,6 +129,7 @@ def test_call_order_and_chunk_arguments(lib):
             assert e.value.status == status, e.value
 
         expect(ss.SS_ERR_BAD_STATE, ss.ss_round_finalize, r, FAKE_Q, 0)            # before candidates
+        expect(ss.SS_ERR_BAD_STATE, ss.ss_round_finalize_chunks, r, [K], [V], [[10, 3]], FAKE_Q)
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_history_chunk, r, K, V, [600, 600])   # > max_chunk_tokens
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_history_chunk, r, K, V, [-1, 3])
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_history_chunk, r, K + 2, V, [10, 3])  # misaligned
@@ -143,6 +148,8 @@ def test_call_order_and_chunk_arguments(lib):
         expect(ss.SS_ERR_BAD_STATE, ss.ss_attend_local_candidates, r, K, V)
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_round_finalize, r, 0, 0)          # null out
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_round_finalize, r, FAKE_Q + 4, 0)  # misaligned out
+        expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_round_finalize_chunks, r, [K], [V], [[10, 3]], 0)
+        expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_round_finalize_chunks, r, [K], [V], [[600, 600]], FAKE_Q)
     finally:
         ss.ss_round_destroy(r)
     ss.ss_round_destroy(None)
@@ -171,3 +178,4 @@ def test_upload_argument_checks(lib):
     with pytest.raises(ss.SpecStreamError) as e:
         ss.ss_upload_chunk(FAKE_WS, FAKE_Q, 0)
     assert e.value.status == ss.SS_ERR_INVALID_ARGUMENT
+
