@@ -2,21 +2,30 @@
 """Benchmark: verify-attention effective KV GB/s and round latency at 32K context.
 
 One step = one whole verification round of the hot path on one GPU: round
-init, every history chunk (8 x 4096 tokens of 16 requests, resident in HBM),
-the Speculative Frontier pass and finalize, on one HIP stream.  Workload: 16
-requests x 32768 history tokens, 32 query / 8 KV heads, d = 128, 6 candidate
-queries per request, bf16 synthetic inputs (seeded, N(0,1)-like).
+init, every history chunk (8 x 4096 tokens of 16 requests, resident in HBM)
+attended in one batched call, the Speculative Frontier call and finalize, on
+one HIP stream: two kernel launches per round (the workspace is zero-filled
+once and reused with counters_zeroed, so no counter clear runs per round).
+Workload: 16 requests x 32768 history tokens, 32 query / 8 KV heads, d = 128,
+6 candidate queries per request, bf16 synthetic inputs (seeded, N(0,1)-like).
 
 value = algorithmic KV bytes per round (sum_b (C_b + n_b) * Hkv * d * 2 * 2)
         x steps / device time of the timed steps.
 
+Order of the run: input generation; 60 rounds in blocks of 10 (`transient`:
+the GPU's power management slows HBM-bound rounds for a few milliseconds
+after it starts streaming, then settles); a device-to-device copy probe; the
+per-launch timing of the round's kernel (`roofline`); per-round percentiles;
+the W warm-up and K timed rounds (`value`); then the secondary measurements.
+
 Extra objects on the JSON line:
-  roofline      dominant kernel (history-chunk MFMA kernel): algorithmic bytes
-                per launch / mean launch time (HIP events on its stream), vs
-                8 TB/s; HBM traffic from committed rocprofv3 counter runs if the
-                kernel source still matches them
-  cpu_baseline  the fp64 oracle timed on this host's cores on a sample of the
-                same workload
+  roofline      the round's dominant kernel (the history attention launch):
+                algorithmic bytes per launch / mean launch time (HIP events
+                on its stream), vs 8 TB/s and vs the copy probe's measured
+                rate; HBM traffic from committed rocprofv3 counter runs if
+                the kernel source still matches them
+  cpu_baseline  the fp64 oracle timed on this host's cores on the same
+                workload; `parity` compares its output with the GPU round's
   streamed      the same round with the history streamed from pinned host
                 memory through the two-slot pipeline (host-link GB/s, overlap)
 
@@ -76,6 +85,48 @@ def time_round_steps(torch, H, b, chunks, stream, steps: int, warmup: int, batch
     return e0.elapsed_time(e1) / 1e3, wall
 
 
+def transient_blocks(torch, H, b, chunks, stream, blocks: int, per_block: int, batch: int):
+    """Mean device time per round of consecutive blocks of back-to-back
+    rounds (events only at block boundaries), right after the inputs were
+    generated: shows how long the GPU takes to settle."""
+    evs = []
+    for _ in range(blocks):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(per_block):
+            H.run_round(b, chunks, stream.cuda_stream, batch=batch)
+        e1.record(stream)
+        evs.append((e0, e1))
+    torch.cuda.synchronize()
+    return [round(e0.elapsed_time(e1) * 1e3 / per_block, 2) for e0, e1 in evs]
+
+
+def copy_probe(torch, stream, nbytes: int = 1 << 31, reps: int = 5):
+    """HBM ceiling check: a plain device-to-device copy of `nbytes` (torch's
+    copy kernel), timed with HIP events; GB/s counts bytes read plus written."""
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    with torch.cuda.stream(stream):
+        dst.copy_(src)
+        ts = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            dst.copy_(src)
+            e1.record(stream)
+            ts.append((e0, e1))
+    torch.cuda.synchronize()
+    t = sorted(e0.elapsed_time(e1) / 1e3 for e0, e1 in ts)
+    del src, dst
+    torch.cuda.empty_cache()
+    med = t[len(t) // 2]
+    return {"bytes_copied": nbytes, "median_ms": round(med * 1e3, 3),
+            "GBs_read_plus_written": round(2 * nbytes / med / 1e9, 1),
+            "best_GBs_read_plus_written": round(2 * nbytes / t[0] / 1e9, 1)}
+
+
 def per_launch_times(torch, ss, b, chunks, stream, rounds: int, batch: int):
     """Device time of each history launch of a round (HIP events recorded on
     the launch's stream around the call; one launch per call here), with the
@@ -109,8 +160,10 @@ def per_launch_times(torch, ss, b, chunks, stream, rounds: int, batch: int):
     return times
 
 
-def cpu_baseline(w, chunks, sample_requests):
-    """fp64 oracle on `sample_requests` whole requests (all heads)."""
+def cpu_baseline(w, chunks, sample_requests, gpu_out=None, gpu_lse=None):
+    """fp64 oracle on `sample_requests` whole requests (all heads); with the
+    GPU round's outputs given, also their parity against the oracle's on
+    every row of the sampled requests."""
     import numpy as np
     import torch
     import oracle
@@ -140,11 +193,26 @@ def cpu_baseline(w, chunks, sample_requests):
                      bf16_bits(w.k_cand(b)), bf16_bits(w.v_cand(b))))
     c0 = os.times()
     t0 = time.perf_counter()
+    refs = []
     for (q, kh, vh, kc, vc) in host:
-        oracle.verify_attention([bf16_bits_to_f64(q)], [bf16_bits_to_f64(kh)], [bf16_bits_to_f64(vh)],
-                                [bf16_bits_to_f64(kc)], [bf16_bits_to_f64(vc)], scale=w.softmax_scale)
+        refs.append(oracle.verify_attention([bf16_bits_to_f64(q)], [bf16_bits_to_f64(kh)], [bf16_bits_to_f64(vh)],
+                                            [bf16_bits_to_f64(kc)], [bf16_bits_to_f64(vc)], scale=w.softmax_scale))
     dt = time.perf_counter() - t0
     c1 = os.times()
+    parity = None
+    if gpu_out is not None:
+        offs = w.row_offsets()
+        go = np.concatenate([gpu_out[offs[b]:offs[b] + w.num_cand[b]].double().cpu().numpy() for b in sample_requests])
+        gl = np.concatenate([gpu_lse[offs[b]:offs[b] + w.num_cand[b]].double().cpu().numpy() for b in sample_requests])
+        ro = np.concatenate([o for o, _ in refs])
+        rl = np.concatenate([l for _, l in refs])
+        parity = {"max_abs": float(f"{np.max(np.abs(go - ro)):.3e}"),
+                  "rel_l2": float(f"{np.linalg.norm(go - ro) / np.linalg.norm(ro):.3e}"),
+                  "lse_max_abs": float(f"{np.max(np.abs(gl - rl)):.3e}"),
+                  "rows_compared": int(go.shape[0] * go.shape[1]), "rows_total": int(w.total_rows * w.num_q_heads),
+                  "bar": {"max_abs": 2e-3, "rel_l2": 1e-3},
+                  "pass": bool(np.max(np.abs(go - ro)) <= 2e-3 and np.linalg.norm(go - ro) <= 1e-3 * np.linalg.norm(ro)),
+                  "what": "the timed round's O and LSE (last round enqueued) against the fp64 oracle"}
     cpu_s = (c1.user - c0.user) + (c1.system - c0.system)   # every thread of this process
     nbytes = sum((w.hist_len[b] + w.num_cand[b]) * w.token_bytes() for b in sample_requests)
     cores = len(os.sched_getaffinity(0))
@@ -164,7 +232,7 @@ def cpu_baseline(w, chunks, sample_requests):
     except Exception:  # pragma: no cover
         one = None
     # cores: the threads the oracle kept busy on average (CPU time / wall time)
-    return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": max(1, round(cpu_s / dt)),
+    return parity, {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": max(1, round(cpu_s / dt)),
             "cpu_seconds": round(cpu_s, 2), "blas_threads": blas_threads,
             "host_cores_available": cores, "kind": "oracle",
             "seconds": round(dt, 3), "one_thread": one,
@@ -268,19 +336,20 @@ def pct(xs, q):
 
 
 def config_table(torch, H, ss, W, stream, layout: int, rounds: int):
-    """In-HBM round of every other configuration (one batched history call;
+    """In-HBM round of every other configuration (one batched history call
+    and finalize, on a zero-filled workspace reused by every round;
     configurations whose history fits the 256 MB last-level cache get a
     512 MiB cache-evicting fill between rounds, outside the timed events)."""
     table = {}
     for cfg in (1, 2, 4, 5):
         w = W.workload(cfg)
         log(f"bench: config {cfg} ({w.name}) in HBM")
-        b = H.RoundBuffers(w, kv_layout=layout)
+        b = H.RoundBuffers(w, kv_layout=layout, counters_zeroed=1)
         chunks = H.hbm_history(w, kv_layout=layout)
         flush = torch.zeros(1 << 27, dtype=torch.int32, device="cuda") if w.history_kv_bytes() < (1 << 28) else None
         torch.cuda.synchronize()
         batch = w.num_chunks
-        round_times(torch, H, b, chunks, stream, 20, batch, flush)   # clocks settle (see --warmup)
+        round_times(torch, H, b, chunks, stream, 20, batch, flush)   # the GPU settles
         t = round_times(torch, H, b, chunks, stream, rounds, batch, flush)
         kv = w.algorithmic_kv_bytes()
         p50 = pct(t, 0.5)
@@ -357,71 +426,33 @@ def full_depth_streamed(torch, H, ss, W, stream, layout: int, layers: int, batch
     return res
 
 
-def ablation(torch, H, ss, W, stream, layout: int):
+def ablation(torch, H, ss, W, stream, layout: int, widths=(5, 6)):
     """Kernel-level analogue of the paper's K1 -> K2 -> K3 ablation (Sec. 5.3.1):
-    K1 restore the whole history to HBM, then attend; K2 stream chunk by chunk
-    through one staging slot (upload and attention alternate); K3 the
-    two-slot pipeline (upload of chunk j+1 overlaps attention on chunk j)."""
+    K1 restore the whole history to HBM, then attend it (one batched call);
+    K2 stream chunk by chunk through one staging slot
+    (upload and attention alternate); K3 the two-slot pipeline (the upload
+    of chunk j+1 overlaps the attention of chunk j).  16K and 32K contexts,
+    1/4/8/16 requests, 5 and 6 candidate rows per request (width q = 4 with
+    the bonus row is the paper's setting)."""
     rows = []
-    for ctx in (16384, 32768):
-        for nreq in (1, 4, 8, 16):
-            w = W.custom([ctx] * nreq, [6] * nreq, num_q_heads=32, num_kv_heads=8, chunk_tokens=4096, seed_base=5)
-            log(f"bench: ablation ctx {ctx} requests {nreq}")
-            host = H.HostHistory(w, kv_layout=layout)
-            b = H.RoundBuffers(w, kv_layout=layout)
-            res = {}
-
-            def vofs(j):   # bytes from a chunk's K to its V in a staging buffer
-                return 2 * w.head_dim if layout == ss.SS_KV_HEAD_MAJOR_KV else host.sizes[j] // 2
-            # K1: restore everything, then one batched attention call
-            dev = [torch.empty(host.sizes[j], dtype=torch.uint8, device="cuda") for j in range(w.num_chunks)]
-            copy = torch.cuda.Stream()
-            done = ss.ss_event_create()
-            try:
-                def k1():
-                    for j in range(w.num_chunks):
-                        ss.ss_upload_chunk(dev[j].data_ptr(), host.chunk_ptr(j), host.sizes[j], copy.cuda_stream,
-                                           None, done if j == w.num_chunks - 1 else None)
-                    r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream.cuda_stream)
-                    try:
-                        half = [vofs(j) for j in range(w.num_chunks)]
-                        ss.ss_attend_history_chunks(r, [dev[j].data_ptr() for j in range(w.num_chunks)],
-                                                    [dev[j].data_ptr() + half[j] for j in range(w.num_chunks)],
-                                                    [w.chunk_lens(j) for j in range(w.num_chunks)], done, None,
-                                                    stream.cuda_stream)
-                        ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream.cuda_stream)
-                        ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream.cuda_stream)
-                    finally:
-                        ss.ss_round_destroy(r)
-
-                def k2():
-                    slot = dev[0]
-                    ready, free = ss.ss_event_create(), ss.ss_event_create()
-                    try:
-                        r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream.cuda_stream)
-                        try:
-                            for j in range(w.num_chunks):
-                                half = vofs(j)
-                                ss.ss_upload_chunk(slot.data_ptr(), host.chunk_ptr(j), host.sizes[j], copy.cuda_stream,
-                                                   free if j else None, ready)
-                                ss.ss_attend_history_chunk(r, slot.data_ptr(), slot.data_ptr() + half, w.chunk_lens(j),
-                                                           ready, free, stream.cuda_stream)
-                            ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream.cuda_stream)
-                            ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream.cuda_stream)
-                        finally:
-                            ss.ss_round_destroy(r)
-                        torch.cuda.synchronize()
-                    finally:
-                        ss.ss_event_destroy(ready)
-                        ss.ss_event_destroy(free)
-
+    for n_cand in widths:
+        for ctx in (16384, 32768):
+            for nreq in (1, 4, 8, 16):
+                w = W.custom([ctx] * nreq, [n_cand] * nreq, num_q_heads=32, num_kv_heads=8, chunk_tokens=4096,
+                             seed_base=5)
+                log(f"bench: ablation ctx {ctx} requests {nreq} candidates {n_cand}")
+                host = H.HostHistory(w, kv_layout=layout)
+                b = H.RoundBuffers(w, kv_layout=layout)
+                copy = torch.cuda.Stream()
+                dev = [torch.empty(max(1, n), dtype=torch.uint8, device="cuda") for n in host.sizes]
+                slot = torch.empty(max(1, host.max_chunk_bytes()), dtype=torch.uint8, device="cuda")
                 pipe = H.Pipeline(host.max_chunk_bytes())
+                res = {"context": ctx, "requests": nreq, "candidates": n_cand, "h2d_bytes": host.total_bytes}
                 try:
-                    def k3():
-                        H.run_round_streamed(b, host, pipe, stream.cuda_stream)
-
-                    for name, fn in (("K1_restore_then_attend", k1), ("K2_stream_no_overlap", k2),
-                                     ("K3_two_slot_pipeline", k3)):
+                    modes = (("K1_restore_then_attend", lambda: H.run_round_restored(b, host, dev, copy, stream.cuda_stream)),
+                             ("K2_stream_one_slot", lambda: H.run_round_single_slot(b, host, slot, copy, stream.cuda_stream)),
+                             ("K3_two_slot_pipeline", lambda: H.run_round_streamed(b, host, pipe, stream.cuda_stream)))
+                    for name, fn in modes:
                         fn()
                         torch.cuda.synchronize()
                         ts = []
@@ -433,22 +464,72 @@ def ablation(torch, H, ss, W, stream, layout: int):
                         res[name + "_ms"] = round(min(ts) * 1e3, 3)
                 finally:
                     pipe.close()
-            finally:
-                ss.ss_event_destroy(done)
-            res.update({"context": ctx, "requests": nreq, "h2d_bytes": host.total_bytes})
-            res["K3_over_K1"] = round(res["K1_restore_then_attend_ms"] / res["K3_two_slot_pipeline_ms"], 3)
-            rows.append(res)
-            del host, b, dev
-            torch.cuda.empty_cache()
+                res["K2_over_K1"] = round(res["K1_restore_then_attend_ms"] / res["K2_stream_one_slot_ms"], 3)
+                res["K3_over_K1"] = round(res["K1_restore_then_attend_ms"] / res["K3_two_slot_pipeline_ms"], 3)
+                res["K3_over_K2"] = round(res["K2_stream_one_slot_ms"] / res["K3_two_slot_pipeline_ms"], 3)
+                rows.append(res)
+                del host, b, dev, slot
+                torch.cuda.empty_cache()
     return rows
+
+
+def width_sweep(torch, H, ss, W, stream, layout: int, rounds: int = 20):
+    """Measured costs of one round at every verification width on config 3's
+    shape (16 requests x 32768 tokens, 32q/8kv): the in-HBM round (one
+    batched history call and finalize) and the streamed round (two-slot pipeline) at n_b = 1..8 rows per
+    request, and the history's upload alone.  These are the transfer and
+    compute inputs of the dynamic-width controller (ss_width_*)."""
+    base = W.workload(3)
+    res = {"workload": "16 requests x 32768 history tokens, 32q/8kv, d=128, chunks of 4096", "widths": {}}
+    host = None
+    for n in range(1, 9):
+        w = W.custom(base.hist_len, [n] * base.B, num_q_heads=32, num_kv_heads=8, chunk_tokens=4096, cfg_id=3)
+        log(f"bench: width sweep, {n} candidate rows per request")
+        b = H.RoundBuffers(w, kv_layout=layout, counters_zeroed=1)
+        chunks = H.hbm_history(w, kv_layout=layout)
+        torch.cuda.synchronize()
+        round_times(torch, H, b, chunks, stream, 10, w.num_chunks)
+        t = round_times(torch, H, b, chunks, stream, rounds, w.num_chunks)
+        del chunks
+        torch.cuda.empty_cache()
+        if host is None:
+            host = H.HostHistory(w, kv_layout=layout)   # the history does not depend on the width
+        pipe = H.Pipeline(host.max_chunk_bytes())
+        try:
+            H.run_round_streamed(b, host, pipe, stream.cuda_stream)
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(3):
+                H.run_round_streamed(b, host, pipe, stream.cuda_stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            t_stream = e0.elapsed_time(e1) / 1e3 / 3
+        finally:
+            pipe.close()
+        res["widths"][str(n)] = {"in_hbm_round_s_p50": pct(t, 0.5), "streamed_round_s": t_stream}
+        del b
+    # the uploads alone, back to back on the copy stream
+    cs = torch.cuda.Stream()
+    slot = torch.empty(host.max_chunk_bytes(), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    c0 = torch.cuda.Event(enable_timing=True)
+    c1 = torch.cuda.Event(enable_timing=True)
+    c0.record(cs)
+    for _ in range(3):
+        for j in range(base.num_chunks):
+            ss.ss_upload_chunk(slot.data_ptr(), host.chunk_ptr(j), host.sizes[j], cs.cuda_stream)
+    c1.record(cs)
+    torch.cuda.synchronize()
+    res["history_upload_s"] = c0.elapsed_time(c1) / 1e3 / 3
+    res["history_bytes"] = host.total_bytes
+    return res
 
 
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    # The GPU's clocks take a few tens of rounds to settle after the input
-    # generation: measured on config 3, 3 warm-up rounds left the timed 20 at
-    # 341-348 us per round, 30 or more at 318-324 us.
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--config", type=int, default=3)
@@ -462,7 +543,7 @@ def main() -> int:
                     help="ss_round_desc.mfma_min_rows (0 = the library's default, always MFMA; "
                          "5 = the fp32 VALU body for up to 4 rows per KV head)")
     ap.add_argument("--batch", type=int, default=0,
-                    help="history chunks per ss_attend_history_chunks call in the timed round "
+                    help="history chunks per history call in the timed round "
                          "(0 = all resident chunks in one call, 1 = one call per chunk)")
     ap.add_argument("--kv-layout", choices=["token", "head", "head-kv"], default="head",
                     help="history chunk layout: token-major [tok][Hkv][d], head-major [Hkv][tok][d] or "
@@ -479,17 +560,21 @@ def main() -> int:
     ap.add_argument("--cpu-sample-requests", type=int, default=16,
                     help="requests of the workload the fp64 oracle is timed on (16 = all of config 3, ~10 s)")
     ap.add_argument("--per-launch-only", action="store_true",
-                    help="only time the history-chunk launches (for profiler runs)")
+                    help="only time the rounds' launches (for profiler runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 1 GiB device-to-device copy (counter calibration)")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the in-HBM rounds of the other configurations")
+    ap.add_argument("--config-rounds", type=int, default=20,
+                    help="timed rounds per other configuration (at least 20)")
     ap.add_argument("--full-depth", type=int, default=0, metavar="LAYERS",
                     help="also time config 5 end to end: LAYERS layers streamed through one pipeline")
     ap.add_argument("--transfer-batch", type=int, default=1,
                     help="chunks per transfer batch in the full-depth streamed round")
     ap.add_argument("--ablation", action="store_true",
-                    help="also run the K1/K2/K3 (restore / stream / stream+prefetch) comparison")
+                    help="only the K1/K2/K3 (restore / stream / stream+prefetch) comparison")
+    ap.add_argument("--width-sweep", action="store_true",
+                    help="only the measured round costs at widths 1..8 (config 3's shape)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); "
@@ -514,13 +599,20 @@ def main() -> int:
         log(f"copy probe: 3 copies of {n} bytes")
         return 0
     ss.load()
+    layout = {"token": ss.SS_KV_TOKEN_MAJOR, "head": ss.SS_KV_HEAD_MAJOR, "head-kv": ss.SS_KV_HEAD_MAJOR_KV}[args.kv_layout]
+    if args.ablation or args.width_sweep:
+        stream = torch.cuda.Stream()
+        if args.ablation:
+            print(json.dumps({"ablation_k1_k2_k3": ablation(torch, H, ss, W, stream, layout)}), flush=True)
+        if args.width_sweep:
+            print(json.dumps({"width_sweep": width_sweep(torch, H, ss, W, stream, layout)}), flush=True)
+        return 0
     w = W.workload(args.config)
     if args.num_cand > 0 or args.num_q_heads > 0:
         w = W.custom(w.hist_len, [args.num_cand] * w.B if args.num_cand > 0 else w.num_cand,
                      num_q_heads=args.num_q_heads or w.num_q_heads, num_kv_heads=w.num_kv_heads,
                      head_dim=w.head_dim, chunk_tokens=w.chunk_tokens, cfg_id=args.config)
     log(f"bench: config {args.config} ({w.name}): generating inputs on the GPU")
-    layout = {"token": ss.SS_KV_TOKEN_MAJOR, "head": ss.SS_KV_HEAD_MAJOR, "head-kv": ss.SS_KV_HEAD_MAJOR_KV}[args.kv_layout]
     if args.streamed_trace:
         b = H.RoundBuffers(w, kv_layout=layout, balance_permille=args.balance_permille)
         host = H.HostHistory(w, kv_layout=layout)
@@ -533,8 +625,9 @@ def main() -> int:
         print(json.dumps({"streamed_trace": {"workload": w.name, "rounds": max(1, args.steps),
                                              "h2d_bytes_per_round": host.total_bytes}}), flush=True)
         return 0
+    # the timed rounds reuse one zero-filled workspace (counters_zeroed): no counter clear per round
     b = H.RoundBuffers(w, split_tokens=args.split_tokens, kv_layout=layout, mfma_min_rows=args.mfma_min_rows,
-                       balance_permille=args.balance_permille)
+                       balance_permille=args.balance_permille, counters_zeroed=1)
     chunks = H.hbm_history(w, kv_layout=layout)
     stream = torch.cuda.Stream()
     torch.cuda.synchronize()
@@ -555,25 +648,30 @@ def main() -> int:
         log(f"per-launch mean {mean * 1e6:.1f} us over {len(times)} launches (batch {batch})")
         return 0
 
-    log(f"bench: timed rounds ({batch} chunk(s) per history call)")
-    dt, wall = time_round_steps(torch, H, b, chunks, stream, args.steps, args.warmup, batch)
-    step_s = dt / args.steps
-    kv_bytes = w.algorithmic_kv_bytes()
-    value = kv_bytes * args.steps / dt / 1e9
-    per_round = round_times(torch, H, b, chunks, stream, args.steps, batch)
-
-    log("bench: per-launch timing of the history kernel")
+    log("bench: rounds right after the input generation, blocks of 10")
+    transient = transient_blocks(torch, H, b, chunks, stream, 6, 10, batch)
+    log("bench: device-to-device copy probe")
+    probe = copy_probe(torch, stream)
+    log("bench: per-launch timing of the round's kernel")
     times = per_launch_times(torch, ss, b, chunks, stream, 5, batch)
     big = max(nb for _, nb in times)
     full = [t for t, nb in times if nb == big]
     launch_s = sum(full) / len(full)
     bytes_per_launch = big
     achieved = bytes_per_launch / launch_s / 1e9
+    per_round = round_times(torch, H, b, chunks, stream, max(20, args.steps), batch)
+
+    log(f"bench: timed rounds ({batch} chunk(s) per history call)")
+    dt, wall = time_round_steps(torch, H, b, chunks, stream, args.steps, args.warmup, batch)
+    step_s = dt / args.steps
+    kv_bytes = w.algorithmic_kv_bytes()
+    value = kv_bytes * args.steps / dt / 1e9
+    out_gpu, lse_gpu = b.out.clone(), b.lse.clone()
 
     per_chunk = None
     if batch != 1:
         log("bench: the same round with one history call per chunk")
-        dt1, _ = time_round_steps(torch, H, b, chunks, stream, args.steps, args.warmup, 1)
+        dt1, _ = time_round_steps(torch, H, b, chunks, stream, args.steps, 5, 1)
         t1 = per_launch_times(torch, ss, b, chunks, stream, 3, 1)
         big1 = max(nb for _, nb in t1)
         l1 = [t for t, nb in t1 if nb == big1]
@@ -592,6 +690,7 @@ def main() -> int:
         except Exception:
             traffic = None
 
+    copy_gbs = probe["GBs_read_plus_written"]
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -610,10 +709,13 @@ def main() -> int:
                         f"history tokens, {w.num_q_heads}q/{w.num_kv_heads}kv heads, d={w.head_dim}, "
                         f"{w.num_chunks} chunks of {w.chunk_tokens}, {w.num_cand[0] if len(set(w.num_cand)) == 1 else 'ragged'} "
                         f"candidate queries, history resident in HBM ({args.kv_layout} chunk layout)",
+            "round_calls": f"init, history calls of {batch} chunk(s), candidates, finalize; zero-filled workspace "
+                           f"reused with counters_zeroed (no counter clear per round)",
             "round_latency_ms": round(step_s * 1e3, 4),
             "round_latency_us_p10_p50_p90": [round(pct(per_round, q) * 1e6, 2) for q in (0.1, 0.5, 0.9)],
             "chunks_per_history_call": batch,
             "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+            "pct_of_measured_copy_rate": round(100.0 * value / copy_gbs, 2),
             "kv_bytes_per_round": kv_bytes,
             "wall_s_timed": round(wall, 4),
         },
@@ -628,13 +730,20 @@ def main() -> int:
             "bytes_per_launch": bytes_per_launch,
             "mean_launch_us": round(launch_s * 1e6, 2),
             "launches_timed": len(full),
+            "measured_copy_GBs": copy_gbs,
+            "frac_of_measured_copy": round(achieved / copy_gbs, 4),
+            "copy_probe": probe,
         },
+        "transient": {"rounds_per_block": 10, "block_mean_round_us": transient,
+                      "what": "the first 60 rounds after input generation, before every other measurement"},
     }
     if per_chunk is not None:
         out["per_chunk_calls"] = per_chunk
     if not args.no_cpu_baseline:
-        log("bench: cpu baseline (fp64 oracle on host cores)")
-        out["cpu_baseline"] = cpu_baseline(w, chunks, list(range(min(w.B, args.cpu_sample_requests))))
+        log("bench: cpu baseline (fp64 oracle on host cores) and parity of the timed round")
+        parity, cb = cpu_baseline(w, chunks, list(range(min(w.B, args.cpu_sample_requests))), out_gpu, lse_gpu)
+        out["cpu_baseline"] = cb
+        out["parity"] = parity
     if not args.no_streamed:
         t_stream, t_h2d, h2d_bytes, same = streamed_round(torch, H, w, b, chunks, stream, 3)
         out["streamed"] = {
@@ -654,12 +763,10 @@ def main() -> int:
     if not args.no_configs and args.config == 3:
         del chunks
         torch.cuda.empty_cache()
-        out["other_configs_in_hbm"] = config_table(torch, H, ss, W, stream, layout, max(5, args.steps // 2))
+        out["other_configs_in_hbm"] = config_table(torch, H, ss, W, stream, layout, max(20, args.config_rounds))
     if args.full_depth > 0:
         out["full_depth_streamed"] = full_depth_streamed(torch, H, ss, W, stream, layout, args.full_depth,
                                                          args.transfer_batch)
-    if args.ablation:
-        out["ablation_k1_k2_k3"] = ablation(torch, H, ss, W, stream, layout)
     print(json.dumps(out), flush=True)
     return 0
 

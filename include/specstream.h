@@ -116,10 +116,9 @@ typedef struct {
                                here from 4096; the result is the same bitwise
                                whichever workgroup attends a unit              */
   int32_t counters_zeroed;  /* the workspace ends with a block of counters
-                               (the balancing tail's claims, the fused
-                               finalize's per-(request, KV head) counts) that
-                               must be zero when a launch that uses them
-                               starts; every such launch leaves them zero.
+                               (the balancing tail's claim counter) that must
+                               be zero when a history launch that uses it
+                               starts; every such launch leaves it zero.
                                0 = the library zeroes the block with a
                                one-wave kernel before the round's first launch
                                that uses it.  1 = the caller guarantees it is
@@ -144,10 +143,9 @@ typedef struct {
 #define SS_KV_HEAD_MAJOR_KV 2
 
 /* Bytes of device workspace a round with this descriptor needs (fp32
- * online-softmax states of every query row, per split slot, then the counter
- * block: 64 words, one of them the balancing tail's claim counter, and one
- * word per (request, KV head) for the fused finalize).  0 if the descriptor
- * is invalid (see ss_last_error). */
+ * online-softmax states of every query row, per split slot, then a 256-byte
+ * counter block whose first word is the balancing tail's claim counter).  0
+ * if the descriptor is invalid (see ss_last_error). */
 size_t ss_round_workspace_bytes(const ss_round_desc *desc);
 
 /* Start a round (paper Sec. 4.2: state (m, l, a) = (-inf, 0, 0) per query and
@@ -157,9 +155,9 @@ size_t ss_round_workspace_bytes(const ss_round_desc *desc);
  * owned by the round until finalize's work has completed.  The empty state
  * is tracked on the host (a split slot is written before it is ever read),
  * so this call enqueues nothing on `stream`; unless desc->counters_zeroed is
- * set, the round's first launch that uses the counter block (a history call
- * with a balancing tail, or ss_round_finalize_chunks) is preceded by a
- * one-wave kernel that zeroes it.
+ * set, the round's first history call with a balancing tail enqueues a
+ * one-wave kernel that zeroes the counter block before its attention
+ * launch.
  * On success *out receives a new handle (free with ss_round_destroy). */
 ss_status ss_round_init(ss_round **out, const ss_round_desc *desc, const void *q,
                         void *workspace, size_t workspace_bytes, hipStream_t stream);
@@ -214,21 +212,6 @@ ss_status ss_attend_local_candidates(ss_round *r, const void *k_cand, const void
  * (m + ln l).  Requires ss_attend_local_candidates to have been called.
  * After finalize the handle accepts no more calls except destroy. */
 ss_status ss_round_finalize(ss_round *r, float *out, float *lse, hipStream_t stream);
-
-/* The round's last history chunks and its finalize in one launch (paper
- * Sec. 4.2: the chunks' Eq. 13 / Eq. 14 updates, then the frontier pass and
- * O = a / l of Eq. 17).  Same result, bitwise, as ss_attend_history_chunks
- * with the same arguments followed by ss_round_finalize: within the launch,
- * the unit that completes a (request, KV head) pair's work merges the
- * pair's slots, attends its frontier and writes its rows of out and lse.
- * Arguments as for those two calls; requires ss_attend_local_candidates to
- * have been called; no history call may follow.  signal_after is recorded
- * after the launch.  A call that does not fit one launch (more than 4096
- * requests, or more units than one launch's tables hold) runs as the two
- * calls.  Uses the workspace's counter block (see counters_zeroed). */
-ss_status ss_round_finalize_chunks(ss_round *r, int32_t num_chunks, const void *const *k, const void *const *v,
-                                   const int32_t *len, hipEvent_t wait_before, hipEvent_t signal_after,
-                                   float *out, float *lse, hipStream_t stream);
 
 /* Free the host handle (never device memory).  Null is ignored.  Call it
  * after enqueueing finalize; enqueued work does not use the handle. */

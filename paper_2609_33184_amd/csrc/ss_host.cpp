@@ -116,8 +116,6 @@ ss_status validate_desc(const ss_round_desc *d) {
     return fail(SS_ERR_INVALID_ARGUMENT, "mfma_min_rows must be in [0, %d]", ss::kMaxValuRows + 1);
   if (d->counters_zeroed != 0 && d->counters_zeroed != 1)
     return fail(SS_ERR_INVALID_ARGUMENT, "counters_zeroed must be 0 or 1");
-  if ((long)d->num_requests * d->num_kv_heads > (1L << 24))
-    return fail(SS_ERR_INVALID_ARGUMENT, "num_requests * num_kv_heads too large");
   if (d->kv_layout != SS_KV_TOKEN_MAJOR && d->kv_layout != SS_KV_HEAD_MAJOR && d->kv_layout != SS_KV_HEAD_MAJOR_KV)
     return fail(SS_ERR_INVALID_ARGUMENT, "kv_layout must be SS_KV_TOKEN_MAJOR, SS_KV_HEAD_MAJOR or SS_KV_HEAD_MAJOR_KV");
   const int G = d->num_q_heads / d->num_kv_heads;
@@ -138,15 +136,12 @@ ss_status validate_desc(const ss_round_desc *d) {
   return SS_OK;
 }
 
-// Workspace: slot states a, m, l, then the counter block: kClaimCounters
-// words (the first is the balancing tail's claim counter), then one
-// finished-unit counter per (request, KV head) for fused finalize launches.
-long counter_words(long B, long Hkv) { return ss::kClaimCounters + B * Hkv; }
-
-size_t workspace_bytes_rows(long R, long B, long Hkv) {
+// Workspace: slot states a, m, l, then the counter block of kClaimCounters
+// words (the first is the balancing tail's claim counter).
+size_t workspace_bytes_rows(long R) {
   const size_t a = align_up((size_t)ss::kNumSlots * R * ss::kHeadDim * sizeof(float), 256);
   const size_t m = align_up((size_t)ss::kNumSlots * R * sizeof(float), 256);
-  return a + 2 * m + align_up((size_t)counter_words(B, Hkv) * sizeof(uint32_t), 256);
+  return a + 2 * m + align_up(ss::kClaimCounters * sizeof(uint32_t), 256);
 }
 
 }  // namespace
@@ -156,8 +151,7 @@ struct ss_round {
   float scale;
   int32_t max_chunk_tokens, split_tokens, mfma_min_rows, kv_layout, tail_permille;
   std::vector<int32_t> n_cand, row_off;
-  uint32_t *counters = nullptr;      // the workspace's counter block: claim counter, then done[B][Hkv]
-  int32_t counter_n = 0;             // words in the block
+  uint32_t *counters = nullptr;      // the workspace's counter block (kClaimCounters words)
   bool counters_ready = false;       // the block is known to be zero (cleared, or the caller said so)
   std::vector<int32_t> slots_used;   // per request: state slots written so far this round
   const uint16_t *q;
@@ -250,7 +244,6 @@ struct Plan {
   std::vector<ss::Item> items;
   std::vector<uint32_t> unit_first{0};
   std::vector<uint8_t> kind;
-  std::vector<int32_t> req;           // request of each unit
   std::vector<uint32_t> wg_first;
   std::vector<int32_t> slots_after;   // per request: slots in use after this call
   size_t tail_first = 0, num_tail = 0;
@@ -324,7 +317,6 @@ bool build_plan(const ss_round *r, int nchunks, const int32_t *len, long W, long
     if (ranges == 0) return;
     plan->unit_first.push_back((uint32_t)plan->items.size());
     plan->kind.push_back((uint8_t)kind_of(r, ub));
-    plan->req.push_back(ub);
     ++slot[ub];
     ranges = 0;
   };
@@ -471,10 +463,6 @@ ss::ChunkParams *base_params(const ss_round *r, int nchunks, const void *const *
   p.claim = nullptr;
   p.tail_first = 0;
   p.num_tail = 0;
-  p.done = nullptr;
-  p.fin_first = 0;
-  p.kc = p.vc = nullptr;
-  p.out = p.lse = nullptr;
   return &p;
 }
 
@@ -500,8 +488,8 @@ hipError_t launch_units(ss::ChunkParams *p, const Plan &plan, F launch) {
     const uint32_t n = plan.unit_first[uend] - i0;
     std::memcpy(p->items, plan.items.data() + i0, n * sizeof(ss::Item));
     for (uint32_t u = u0; u < uend; ++u)
-      p->units[u - u0] = ss::pack_unit(plan.unit_first[u] - i0, plan.unit_first[u + 1] - plan.unit_first[u],
-                                       plan.kind[u], (uint32_t)plan.req[u]);
+      p->units[u - u0] = (plan.unit_first[u] - i0) | ((plan.unit_first[u + 1] - plan.unit_first[u]) << 16) |
+                         ((uint32_t)plan.kind[u] << 24);
     for (size_t w = w0; w <= w1; ++w) p->wg_first[w - w0] = (uint16_t)(plan.wg_first[w] - u0);
     p->num_items = (int32_t)n;
     p->num_units = (int32_t)(uend - u0);
@@ -534,7 +522,7 @@ hipError_t launch_items(P *p, const std::vector<ss::Item> &items, F launch) {
 // at zero, so one clear serves the whole round.
 ss_status ensure_counters(ss_round *r, hipStream_t stream) {
   if (r->counters_ready) return SS_OK;
-  const hipError_t e = ss::launch_clear_counters(r->counters, r->counter_n, stream);
+  const hipError_t e = ss::launch_clear_counters(r->counters, ss::kClaimCounters, stream);
   if (e != hipSuccess) {
     r->failed = true;
     return hip_fail(e, "counter clear launch");
@@ -600,17 +588,13 @@ ss_status attend_history(ss_round *r, int nchunks, const void *const *k, const v
   return enqueue_history(r, nchunks, k, v, pr, wait_before, signal_after, stream);
 }
 
-// Finalize item of request b: the slots to merge and, for a fused launch,
-// the number of the request's units in the launch.
-ss::Item fin_item(const ss_round *r, int b, int slots, int units) {
+// Finalize item of request b: the slots its history calls wrote.
+ss::Item fin_item(const ss_round *r, int b) {
   ss::Item it{};
   it.tok_begin = 0;
-  it.tok_count = slots;
+  it.tok_count = r->slots_used[b];
   it.q_row0 = r->row_off[b];
   it.n_cand = (uint8_t)r->n_cand[b];
-  it.chunk = 0;
-  it.slot = (uint8_t)units;
-  it.flags = 0;
   return it;
 }
 
@@ -626,7 +610,7 @@ bool check_out(float *out, float *lse, ss_status *s) {
   return true;
 }
 
-// The finalize kernel: one workgroup per (KV head, request).
+// The finalize kernel: one wave per query row.
 ss_status enqueue_finalize(ss_round *r, float *out, float *lse, hipStream_t stream) {
   static thread_local ss::FinalParams p;
   p.kc = r->kc;
@@ -640,105 +624,13 @@ ss_status enqueue_finalize(ss_round *r, float *out, float *lse, hipStream_t stre
   p.G = r->G;
   p.scale_log2 = r->scale * 1.4426950408889634f;
   std::vector<ss::Item> items(r->B);
-  for (int b = 0; b < r->B; ++b) items[b] = fin_item(r, b, r->slots_used[b], 0);
+  for (int b = 0; b < r->B; ++b) items[b] = fin_item(r, b);
   const hipError_t e = launch_items(&p, items, [&](const ss::FinalParams &q) { return ss::launch_finalize(q, stream); });
   if (e != hipSuccess) {
     r->failed = true;
     return hip_fail(e, "finalize kernel launch");
   }
   r->finalized = true;
-  return SS_OK;
-}
-
-// The plan of a history call whose launch also finalizes the round: every
-// request gets its finalize item (after the units' items), and a request
-// without tokens in the call gets a kUnitFinal unit, spread over the
-// workgroups' lists.  False if the result does not fit one launch.
-bool make_fused_plan(const ss_round *r, const Plan &plan, Plan *out, size_t *fin_first) {
-  if (r->B > ss::kMaxFusedRequests || !fits_one_launch(plan)) return false;
-  const size_t W = plan.wg_first.size() - 1;
-  std::vector<int> units(r->B, 0);
-  for (size_t u = 0; u < plan.units(); ++u) ++units[plan.req[u]];
-  std::vector<std::vector<int>> extra(W);
-  size_t k = 0;
-  for (int b = 0; b < r->B; ++b)
-    if (units[b] == 0) extra[k++ % W].push_back(b);
-  Plan q;
-  q.items = plan.items;
-  q.slots_after = plan.slots_after;
-  auto copy_unit = [&](size_t u) {
-    q.unit_first.push_back(plan.unit_first[u + 1] - plan.unit_first[u] + q.unit_first.back());
-    q.kind.push_back(plan.kind[u]);
-    q.req.push_back(plan.req[u]);
-  };
-  for (size_t w = 0; w < W; ++w) {
-    q.wg_first.push_back((uint32_t)q.units());
-    for (uint32_t u = plan.wg_first[w]; u < plan.wg_first[w + 1]; ++u) copy_unit(u);
-    for (int b : extra[w]) {
-      q.unit_first.push_back(q.unit_first.back());   // no items
-      q.kind.push_back((uint8_t)ss::kUnitFinal);
-      q.req.push_back(b);
-    }
-  }
-  q.wg_first.push_back((uint32_t)q.units());
-  q.tail_first = q.units();
-  for (size_t u = plan.tail_first; u < plan.units(); ++u) copy_unit(u);
-  q.num_tail = plan.num_tail;
-  *fin_first = q.items.size();
-  for (int b = 0; b < r->B; ++b) q.items.push_back(fin_item(r, b, q.slots_after[b], units[b] > 0 ? units[b] : 1));
-  if (q.units() > (size_t)ss::kMaxUnits || q.items.size() > (size_t)ss::kMaxItems) return false;
-  *out = std::move(q);
-  return true;
-}
-
-// The round's last history call with the finalize fused into its launch
-// (or, where the call does not fit one fused launch, the history launches
-// followed by the finalize kernel).
-ss_status enqueue_history_final(ss_round *r, int nchunks, const void *const *k, const void *const *v,
-                                const Prepared &pr, hipEvent_t wait_before, hipEvent_t signal_after, float *out,
-                                float *lse, hipStream_t stream) {
-  Plan plan;
-  size_t fin_first = 0;
-  if (pr.total == 0 || !make_fused_plan(r, pr.plan, &plan, &fin_first)) {
-    ss_status s = enqueue_history(r, nchunks, k, v, pr, wait_before, signal_after, stream);
-    if (s != SS_OK) return s;
-    return enqueue_finalize(r, out, lse, stream);
-  }
-  hipError_t e;
-  if (wait_before != nullptr && (e = hipStreamWaitEvent(stream, wait_before, 0)) != hipSuccess)
-    return hip_fail(e, "hipStreamWaitEvent (history)");
-  ss_status s = ensure_counters(r, stream);
-  if (s != SS_OK) return s;
-  ss::ChunkParams *p = base_params(r, nchunks, k, v, pr.tot);
-  const size_t W = plan.wg_first.size() - 1;
-  for (size_t u = 0; u < plan.units(); ++u)
-    p->units[u] = ss::pack_unit(plan.unit_first[u], plan.unit_first[u + 1] - plan.unit_first[u], plan.kind[u],
-                                (uint32_t)plan.req[u]);
-  for (size_t w = 0; w <= W; ++w) p->wg_first[w] = (uint16_t)plan.wg_first[w];
-  std::memcpy(p->items, plan.items.data(), plan.items.size() * sizeof(ss::Item));
-  p->num_items = (int32_t)plan.items.size();
-  p->num_units = (int32_t)plan.units();
-  p->num_wgs = (int32_t)W;
-  p->tail_first = plan.num_tail > 0 ? (int32_t)plan.tail_first : 0;
-  p->num_tail = (int32_t)plan.num_tail;
-  p->claim = r->counters;
-  p->done = r->counters + ss::kClaimCounters;
-  p->fin_first = (int32_t)fin_first;
-  p->kc = r->kc;
-  p->vc = r->vc;
-  p->out = out;
-  p->lse = lse;
-  e = ss::launch_chunk(*p, stream);
-  if (e != hipSuccess) {
-    r->failed = true;
-    return hip_fail(e, "history chunk kernel launch (fused finalize)");
-  }
-  r->slots_used = plan.slots_after;
-  r->finalized = true;
-  if (signal_after != nullptr && (e = hipEventRecord(signal_after, stream)) != hipSuccess) {
-    r->failed = true;
-    return hip_fail(e, "hipEventRecord (history)");
-  }
   return SS_OK;
 }
 
@@ -808,7 +700,7 @@ size_t ss_round_workspace_bytes(const ss_round_desc *desc) {
   if (validate_desc(desc) != SS_OK) return 0;
   long R = 0;
   for (int b = 0; b < desc->num_requests; ++b) R += (long)desc->num_cand[b] * desc->num_q_heads;
-  return workspace_bytes_rows(R, desc->num_requests, desc->num_kv_heads);
+  return workspace_bytes_rows(R);
 }
 
 }  // extern "C"
@@ -827,7 +719,7 @@ ss_status init_round(ss_round **out, const ss_round_desc *desc, const void *q, v
   if (q == nullptr || !aligned(q, 16)) return fail(SS_ERR_INVALID_ARGUMENT, "q must be non-null and 16-byte aligned");
   long R = 0;
   for (int b = 0; b < desc->num_requests; ++b) R += (long)desc->num_cand[b] * desc->num_q_heads;
-  const size_t need = workspace_bytes_rows(R, desc->num_requests, desc->num_kv_heads);
+  const size_t need = workspace_bytes_rows(R);
   if (workspace == nullptr || !aligned(workspace, 256))
     return fail(SS_ERR_WORKSPACE, "workspace must be non-null and 256-byte aligned");
   if (workspace_bytes < need)
@@ -864,7 +756,6 @@ ss_status init_round(ss_round **out, const ss_round_desc *desc, const void *q, v
   r->st.m = reinterpret_cast<float *>(ws + a_bytes);
   r->st.l = reinterpret_cast<float *>(ws + a_bytes + m_bytes);
   r->counters = reinterpret_cast<uint32_t *>(ws + a_bytes + 2 * m_bytes);
-  r->counter_n = (int32_t)counter_words(r->B, r->Hkv);
   r->counters_ready = desc->counters_zeroed != 0;
   r->tail_permille = desc->balance_permille;
   r->st.R = (int32_t)R;
@@ -926,21 +817,6 @@ ss_status ss_round_finalize(ss_round *r, float *out, float *lse, hipStream_t str
     if (!r->cand_done) return fail(SS_ERR_BAD_STATE, "finalize before ss_attend_local_candidates");
     if (!check_out(out, lse, &s)) return s;
     return enqueue_finalize(r, out, lse, stream);
-  });
-}
-
-ss_status ss_round_finalize_chunks(ss_round *r, int32_t num_chunks, const void *const *k, const void *const *v,
-                                   const int32_t *len, hipEvent_t wait_before, hipEvent_t signal_after, float *out,
-                                   float *lse, hipStream_t stream) {
-  return guarded([&]() -> ss_status {
-    ss_status s = check_round(r);
-    if (s != SS_OK) return s;
-    if (!r->cand_done) return fail(SS_ERR_BAD_STATE, "finalize before ss_attend_local_candidates");
-    if (!check_out(out, lse, &s)) return s;
-    Prepared pr;
-    s = prepare_history(r, num_chunks, k, v, len, &pr);
-    if (s != SS_OK) return s;
-    return enqueue_history_final(r, num_chunks, k, v, pr, wait_before, signal_after, out, lse, stream);
   });
 }
 

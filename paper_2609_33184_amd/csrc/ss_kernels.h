@@ -18,8 +18,7 @@ constexpr int kWaves = 4;           // waves per workgroup of the chunk kernels
 constexpr int kMaxCand = 8;         // candidates per request (k_b + 1)
 constexpr int kMaxValuRows = 4;     // rows per KV head the VALU chunk kernel handles
 constexpr int kMaxRows = 64;        // rows per KV head the MFMA chunk kernels handle
-constexpr int kClaimCounters = 64;  // words before the per-(request, KV head) counters (one used: the claim counter)
-constexpr int kMaxFusedRequests = 4096;   // requests of a history launch fused with finalize (12-bit unit field)
+constexpr int kClaimCounters = 64;  // words of the workspace's counter block (the first is the claim counter)
 
 // Unit kinds: the chunk kernel body that attends a unit (rows per KV head
 // M = n_b * G: <= 4 on the VALU path, else MFMA with ceil(M / 16) blocks).
@@ -28,15 +27,6 @@ constexpr int kUnitMfma1 = 1;
 constexpr int kUnitMfma2 = 2;
 constexpr int kUnitMfma3 = 3;       // wide units (row-split body): only the wide kernel runs them
 constexpr int kUnitMfma4 = 4;
-constexpr int kUnitFinal = 5;       // no tokens: only the finalize epilogue of a fused launch
-
-// Unit table entry: items [i0, i0 + nit) (nit = 0 for kUnitFinal) attended by
-// body `kind` for request `req` (the request index is read by fused launches
-// only).
-constexpr uint32_t pack_unit(uint32_t i0, uint32_t nit, uint32_t kind, uint32_t req) {
-  return (i0 & 0xfffu) | ((nit & 0x1fu) << 12) | ((kind & 0x7u) << 17) | ((req & 0xfffu) << 20);
-}
-static_assert(kMaxItems <= 4096 && kMaxChain <= 31 && kMaxFusedRequests <= 4096, "unit table fields");
 
 // Item flag: the slot has not been written in this round yet, so the kernel
 // stores its result instead of merging with (uninitialised) workspace.
@@ -49,9 +39,7 @@ constexpr int kSlotFresh = 1;
 // state that is folded into split slot `slot`; every item of a chain carries
 // the same q_row0, n_cand, slot and flags.
 // Finalize item: one request; tok_count = number of slots written by
-// history calls (slots >= that are empty); in a fused launch `slot` holds the
-// number of the request's units in the launch (each runs once per KV head),
-// other token fields unused.
+// history calls (slots >= that are empty), other token fields unused.
 struct Item {
   int32_t tok_begin;
   int32_t tok_count;
@@ -101,16 +89,6 @@ struct ChunkHeader {
   uint32_t *claim;
   int32_t tail_first;
   int32_t num_tail;
-  // Fused finalize (done != null): done[req * Hkv + g] counts the finished
-  // units of (request, KV head); the unit that completes the count (items
-  // [fin_first + req]'s `slot` units) sets it back to zero and finalizes the
-  // pair's rows: slot merge, Speculative Frontier, O = a / l and LSE.
-  uint32_t *done;
-  int32_t fin_first;
-  const uint16_t *kc;   // bf16 candidate K [sum n_b, Hkv, d]
-  const uint16_t *vc;   // bf16 candidate V
-  float *out;           // fp32 [sum n_b, Hq, d]
-  float *lse;           // fp32 [sum n_b, Hq] or null
 };
 
 template <int MaxUnits, int MaxItems, int MaxWgs>
@@ -118,7 +96,8 @@ struct ChunkParamsT : ChunkHeader {
   static constexpr int kUnits = MaxUnits;
   static constexpr int kItems = MaxItems;
   static constexpr int kWgs = MaxWgs;
-  // unit table (pack_unit): items, body and request of each unit
+  // unit u = items [units[u] & 0xffff, + ((units[u] >> 16) & 0xff)), 1..kMaxChain
+  // items, attended by the body units[u] >> 24 (kUnitValu / kUnitMfma1..4)
   uint32_t units[MaxUnits];
   // workgroup w (of every KV head) attends units [wg_first[w], wg_first[w + 1]) in order
   uint16_t wg_first[MaxWgs + 1];
@@ -146,11 +125,9 @@ struct FinalParamsT : FinalHeader {
 using FinalParams = FinalParamsT<kMaxItems>;
 
 // Launch wrappers; return hipGetLastError() of the launch.
-// History units of every kind, grid (Hkv, num_wgs); with p.done set, the
-// launch also finalizes every request (fused finalize).
+// History units of every kind, grid (Hkv, num_wgs).
 hipError_t launch_chunk(const ChunkParams &p, hipStream_t s);
-// Speculative Frontier pass fused with the split-slot merge and O = a / l,
-// one workgroup per (KV head, request), grid (Hkv, num_items).
+// Speculative Frontier pass fused with the split-slot merge and O = a / l.
 hipError_t launch_finalize(const FinalParams &p, hipStream_t s);
 // Zero n counters (a kernel rather than a memset node, so the call can be
 // captured in a graph).

@@ -909,186 +909,6 @@ static_assert(MfmaLds<1>::kBytes <= kChunkLdsBytes, "LDS sizes");
 static_assert(kRowsLdsBytes <= kChunkLdsBytes && 2 * kChunkLdsBytes <= 160 * 1024, "LDS sizes");
 
 // ---------------------------------------------------------------------------
-// Finalize of one (request, KV head) pair: for each of its M = n_b * G query
-// rows (candidate i, head h = g G + r % G)
-//   * attend the Speculative Frontier: candidate keys j <= i of the same
-//     request, causal by absolute position (Sec. 4.2, GPU-resident pass),
-//   * merge the split slots the history calls wrote (Eq. 14; the slot count
-//     comes from the host, unwritten slots are never read),
-//   * write O = a / l and LSE = m ln 2 + ln l (Eq. 17).
-// The pair's candidate K and V rows (shared by all its rows) are staged in
-// LDS once.  Sixteen threads per row, 8 d values each, 16 rows per pass of
-// the 256 threads.  A pass issues its query and first slot loads before any
-// use (the first pass's before the candidate staging); the <= 8 candidate
-// dot products are summed over the row's sixteen threads as independent
-// chains; the frontier terms come first, then each group of kFinGroup slots
-// is folded in with the rescaled update of Eq. 14.  The finalize kernel and
-// the fused epilogue of the history kernel both run this function, so their
-// results are bitwise equal.
-// ---------------------------------------------------------------------------
-constexpr int kFinGroup = 4;
-constexpr int kFinLdsBytes = 2 * kMaxCand * kRowBytes;   // candidate K rows, then V rows
-
-// Fields of a finalize item, read as whole dwords (see item_chunk).
-struct FinItem {
-  int nslot, q_row0, n_cand, units;
-};
-__device__ __forceinline__ FinItem fin_item(const Item &it) {
-  uint32_t w[4];
-  __builtin_memcpy(w, &it, sizeof w);
-  return FinItem{(int)w[1], (int)w[2], (int)(w[3] & 0xffu), (int)((w[3] >> 16) & 0xffu)};
-}
-static_assert(offsetof(Item, tok_count) == 4 && offsetof(Item, q_row0) == 8 && offsetof(Item, n_cand) == 12 &&
-                  offsetof(Item, slot) == 14,
-              "Item layout");
-
-template <typename P>
-__device__ __forceinline__ void finalize_pair(const P &p, const FinItem &fi, int g, int tx, unsigned char *lds) {
-  const int M = fi.n_cand * p.G;
-  const int part = tx & 15;                       // d values [8 part, 8 part + 8)
-  u32x4_t q;
-  float ms[kFinGroup], ls[kFinGroup];
-  f32x4_t as[kFinGroup][2];
-  int row = 0, i = 0;
-  auto load_row = [&](int r0) {                   // this thread's row of the pass and its query
-    const int r = r0 + (tx >> 4);
-    const int rr = r < M ? r : 0;                 // idle threads redo row 0 and store nothing
-    i = rr / p.G;
-    row = (fi.q_row0 + i) * p.Hq + g * p.G + (rr - i * p.G);
-    q = reinterpret_cast<const u32x4_t *>(p.q + (size_t)row * kHeadDim)[part];
-  };
-  auto load_group = [&](int s0) {
-#pragma unroll
-    for (int u = 0; u < kFinGroup; ++u) {
-      ms[u] = kNegInf;
-      ls[u] = 0.f;
-      as[u][0] = as[u][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      if (s0 + u < fi.nslot) {
-        const size_t idx = (size_t)(s0 + u) * p.st.R + row;
-        ms[u] = p.st.m[idx];
-        ls[u] = p.st.l[idx];
-        const f32x4_t *ap = reinterpret_cast<const f32x4_t *>(p.st.a + idx * kHeadDim) + 2 * part;
-        as[u][0] = ap[0];
-        as[u][1] = ap[1];
-      }
-    }
-  };
-  // candidate rows -> LDS: thread tx < 32 n_b loads 16 bytes (j = tx / 32,
-  // K for (tx / 16) even, V for odd, chunk tx % 16)
-  const int cj = tx >> 5, cv = (tx >> 4) & 1, cc = tx & 15;
-  const bool cld = cj < fi.n_cand;
-  u32x4_t cand = u32x4_t{0u, 0u, 0u, 0u};
-  if (cld) {
-    const uint16_t *src = (cv ? p.vc : p.kc) + ((size_t)(fi.q_row0 + cj) * p.Hkv + g) * kHeadDim;
-    cand = reinterpret_cast<const u32x4_t *>(src)[cc];
-  }
-  load_row(0);
-  load_group(0);
-  if (cld) *reinterpret_cast<u32x4_t *>(lds + cv * (kMaxCand * kRowBytes) + cj * kRowBytes + 16 * cc) = cand;
-  __syncthreads();
-
-  for (int r0 = 0; r0 < M; r0 += 16) {
-    if (r0 > 0) {
-      load_row(r0);
-      load_group(0);
-    }
-    // frontier scores: partial dots over this thread's 8 values, summed over
-    // the row's sixteen threads
-    float x[kMaxCand];
-#pragma unroll
-    for (int j = 0; j < kMaxCand; ++j) {
-      const u32x4_t kw = reinterpret_cast<const u32x4_t *>(lds + j * kRowBytes)[part];
-      float d = 0.f;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        d = fmaf(bf16_lo(q[e]), bf16_lo(kw[e]), d);
-        d = fmaf(bf16_hi(q[e]), bf16_hi(kw[e]), d);
-      }
-      x[j] = d;
-    }
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1)
-#pragma unroll
-      for (int j = 0; j < kMaxCand; ++j) x[j] += __shfl_xor(x[j], off);
-    float m = kNegInf;
-#pragma unroll
-    for (int j = 0; j < kMaxCand; ++j) {
-      x[j] = j <= i ? x[j] * p.scale_log2 : kNegInf;   // candidates past n_b read unused LDS: discarded here
-      m = fmaxf(m, x[j]);
-    }
-    // m is finite: every query sees candidate 0
-    float l = 0.f;
-    float a[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) a[e] = 0.f;
-#pragma unroll
-    for (int j = 0; j < kMaxCand; ++j) {
-      if (j <= i) {
-        const float pj = exp2_fast(x[j] - m);
-        l += pj;
-        const u32x4_t vw = reinterpret_cast<const u32x4_t *>(lds + (kMaxCand + j) * kRowBytes)[part];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          a[2 * e] = fmaf(pj, bf16_lo(vw[e]), a[2 * e]);
-          a[2 * e + 1] = fmaf(pj, bf16_hi(vw[e]), a[2 * e + 1]);
-        }
-      }
-    }
-    for (int s0 = 0; s0 < fi.nslot; s0 += kFinGroup) {
-      if (s0 > 0) load_group(s0);
-      float mg = m;
-#pragma unroll
-      for (int u = 0; u < kFinGroup; ++u) mg = fmaxf(mg, ms[u]);
-      const float c = exp2_fast(m - mg);          // both finite
-      l *= c;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) a[e] *= c;
-      m = mg;
-#pragma unroll
-      for (int u = 0; u < kFinGroup; ++u) {
-        const float f = exp2_fast(ms[u] - m);     // 0 for an unused slot (m = -inf)
-        l = fmaf(f, ls[u], l);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          a[e] = fmaf(f, as[u][0][e], a[e]);
-          a[4 + e] = fmaf(f, as[u][1][e], a[4 + e]);
-        }
-      }
-    }
-    if (r0 + (tx >> 4) < M) {
-      const float inv = 1.0f / l;
-      f32x4_t *op = reinterpret_cast<f32x4_t *>(p.out + (size_t)row * kHeadDim) + 2 * part;
-      op[0] = f32x4_t{a[0] * inv, a[1] * inv, a[2] * inv, a[3] * inv};
-      op[1] = f32x4_t{a[4] * inv, a[5] * inv, a[6] * inv, a[7] * inv};
-      if (p.lse != nullptr && part == 0) p.lse[row] = m * 0.69314718055994531f + logf(l);
-    }
-  }
-}
-
-// After a unit of a fused launch: count it for its (request, KV head); the
-// unit that completes the count sets the counter back to zero and finalizes
-// the pair.  Every thread fences its own slot stores before the count
-// (device-scope release), and the finalizing workgroup fences before it
-// reads the other units' slots (device-scope acquire): the units of one
-// pair run on any of the XCDs, whose L2 caches are not coherent with each
-// other without these fences.
-template <typename P>
-__device__ __forceinline__ void unit_done(const P &p, int req, int g, int tx, uint32_t *count_sh,
-                                          unsigned char *lds) {
-  __threadfence();
-  __syncthreads();
-  uint32_t *ctr = p.done + (size_t)req * p.Hkv + g;
-  if (tx == 0) *count_sh = atomicAdd(ctr, 1u);
-  __syncthreads();
-  const FinItem fi = fin_item(p.items[p.fin_first + req]);
-  const uint32_t c = __builtin_amdgcn_readfirstlane(*count_sh);
-  if (c + 1u != (uint32_t)fi.units) return;
-  if (tx == 0) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __threadfence();
-  finalize_pair(p, fi, g, tx, lds);
-}
-
-// ---------------------------------------------------------------------------
 // History kernel: one launch for every unit of a call.  Workgroup =
 // (kv head, w) = (blockIdx.x, blockIdx.y) first attends the units of its own
 // list in order (the host gives every workgroup an equal share of the
@@ -1110,19 +930,13 @@ __device__ __forceinline__ void unit_done(const P &p, int req, int g, int tx, ui
 // launch makes num_tail * Hkv + (workgroups) claims; the one that receives
 // the last number sets the counter back to zero for the next launch.
 // Claims are compared without sign: a counter that is not zero at launch
-// (a violated workspace contract) gives large numbers, which end the loop.
-//
-// Fused (the round's last history call with finalize): after each unit the
-// workgroup counts the unit for its (request, KV head) pair, and the unit
-// that completes a pair's count finalizes the pair (unit_done).  Requests
-// without tokens in the launch get a unit of kind kUnitFinal that only
-// finalizes.
+// (garbage, or a broken workspace promise) gives large numbers, which end
+// the loop instead of indexing outside the tail.
 // ---------------------------------------------------------------------------
-template <bool Wide, bool Fused, typename P>
+template <bool Wide, typename P>
 __global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[kChunkLdsBytes];
   __shared__ uint32_t claim_sh;
-  __shared__ uint32_t count_sh;
   const int u0 = p.wg_first[blockIdx.y];
   const int u1 = p.wg_first[blockIdx.y + 1];
   const uint32_t nclaims = (uint32_t)p.num_tail * (uint32_t)p.Hkv;
@@ -1158,34 +972,135 @@ __global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
     int tx = threadIdx.x;
     asm volatile("" : "+v"(tx));
     const uint32_t unit = p.units[uidx];
-    const int i0 = unit & 0xfff;
-    const int nit = (unit >> 12) & 0x1f;
-    const int kind = (unit >> 17) & 0x7;
-    if (kind == kUnitFinal) {
-      // no tokens of this request in the launch: only the finalize
-    } else if (Wide && kind >= kUnitMfma3) {
-      if constexpr (Wide) rows_unit(p, smem, i0, nit, tx, g);
-    } else if (kind == kUnitMfma2) {
-      mfma_unit<2>(p, smem, i0, nit, tx, g);
-    } else if (kind == kUnitMfma1) {
-      mfma_unit<1>(p, smem, i0, nit, tx, g);
-    } else {
-      valu_unit<kMaxValuRows>(p, reinterpret_cast<float *>(smem), i0, nit, tx, g);
+    const int i0 = unit & 0xffff;
+    const int nit = (unit >> 16) & 0xff;
+    const int kind = unit >> 24;
+    if constexpr (Wide) {
+      if (kind >= kUnitMfma3) {
+        rows_unit(p, smem, i0, nit, tx, g);
+        continue;
+      }
     }
-    if constexpr (Fused) unit_done(p, (int)(unit >> 20), g, tx, &count_sh, smem);
+    if (kind == kUnitMfma2)
+      mfma_unit<2>(p, smem, i0, nit, tx, g);
+    else if (kind == kUnitMfma1)
+      mfma_unit<1>(p, smem, i0, nit, tx, g);
+    else
+      valu_unit<kMaxValuRows>(p, reinterpret_cast<float *>(smem), i0, nit, tx, g);
   }
 }
 
-__global__ void __launch_bounds__(256) clear_counters_kernel(uint32_t *c, int n) {
-  for (int i = threadIdx.x; i < n; i += 256) c[i] = 0u;
+__global__ void __launch_bounds__(64) clear_counters_kernel(uint32_t *c, int n) {
+  for (int i = threadIdx.x; i < n; i += 64) c[i] = 0u;
 }
 
-// Finalize of a round whose history calls ran without the fused epilogue:
-// workgroup (g, b) finalizes KV head g of request b (grid (Hkv, requests)).
+// ---------------------------------------------------------------------------
+// Finalize: for every query row (request b, candidate i, head h)
+//   * attend the Speculative Frontier: candidate keys j <= i of the same
+//     request, causal by absolute position (Sec. 4.2, GPU-resident pass),
+//   * merge the split slots the history calls wrote (Eq. 14; slot count per
+//     request from the host, unwritten slots are never read),
+//   * write O = a / l and LSE = m ln 2 + ln l (Eq. 17).
+// One wave per row (grid.y covers a request's rows, 4 per workgroup); lane l
+// holds d = 2l, 2l+1.  The kernel is latency-bound, so a row costs one
+// memory round trip: every load is issued before any use (the query, the
+// visible candidates' K/V, each slot's m and l - lane s loads slot s - and
+// every slot's a values).  The row's maximum over the frontier scores and
+// the slot maxima then gives each term its scale 2^(m_s - m*) once (Eq. 14
+// applied to all pieces together), so the slots need no step-by-step
+// rescaling.  Slot loads past the request's count go through empty buffer
+// resources or offsets past the end and read zeros.
+// ---------------------------------------------------------------------------
 template <typename P>
-__global__ void __launch_bounds__(256, 2) finalize_kernel(const P p) {
-  __shared__ __attribute__((aligned(16))) unsigned char lds[kFinLdsBytes];
-  finalize_pair(p, fin_item(p.items[blockIdx.y]), blockIdx.x, threadIdx.x, lds);
+__global__ void __launch_bounds__(256) finalize_kernel(const P p) {
+  const int w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const Item it = p.items[blockIdx.x];
+  const int r = blockIdx.y * kWaves + w;          // local row = i * Hq + h
+  if (r >= it.n_cand * p.Hq) return;
+  const int i = r / p.Hq;
+  const int h = r - i * p.Hq;
+  const int g = h / p.G;
+  const int row = __builtin_amdgcn_readfirstlane(it.q_row0 * p.Hq + r);   // (off_b + i) * Hq + h
+  const int nslot = it.tok_count;
+
+  const uint32_t qw = reinterpret_cast<const uint32_t *>(p.q + (size_t)row * kHeadDim)[lane];
+  uint32_t kw[kMaxCand], vw[kMaxCand];
+#pragma unroll
+  for (int j = 0; j < kMaxCand; ++j) {
+    kw[j] = 0;
+    vw[j] = 0;
+    if (j <= i) {
+      const size_t kv = ((size_t)(it.q_row0 + j) * p.Hkv + g) * kHeadDim;
+      kw[j] = reinterpret_cast<const uint32_t *>(p.kc + kv)[lane];
+      vw[j] = reinterpret_cast<const uint32_t *>(p.vc + kv)[lane];
+    }
+  }
+  // slot s's m and l in lane s (offsets past the array read zero)
+  const __amdgpu_buffer_rsrc_t mrs = __builtin_amdgcn_make_buffer_rsrc(
+      p.st.m, (short)0, (int)((uint32_t)kNumSlots * (uint32_t)p.st.R * 4), kBufferFlags);
+  const __amdgpu_buffer_rsrc_t lrs = __builtin_amdgcn_make_buffer_rsrc(
+      p.st.l, (short)0, (int)((uint32_t)kNumSlots * (uint32_t)p.st.R * 4), kBufferFlags);
+  const uint32_t moff = lane < nslot ? ((uint32_t)lane * (uint32_t)p.st.R + (uint32_t)row) * 4 : 0xfffffff0u;
+  const float m_lane = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(mrs, moff, 0, 0));
+  const float l_lane = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(lrs, moff, 0, 0));
+  // every slot's a values of this row: slot s through a resource over the
+  // row's 512 bytes in that slot (empty past the count)
+  float2 as[kNumSlots];
+#pragma unroll
+  for (int s = 0; s < kNumSlots; ++s) {
+    const float *base = p.st.a + ((size_t)s * p.st.R + row) * kHeadDim;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(base), (short)0, s < nslot ? kRowBytes * 2 : 0, kBufferFlags);
+    const uint64_t v = __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(rs, (uint32_t)lane * 8, 0, 0));
+    as[s] = __builtin_bit_cast(float2, v);
+  }
+
+  // frontier scores: the <= 8 dot products reduced as independent chains
+  const float q0 = bf16_lo(qw), q1 = bf16_hi(qw);
+  float x[kMaxCand];
+#pragma unroll
+  for (int j = 0; j < kMaxCand; ++j) x[j] = fmaf(q0, bf16_lo(kw[j]), q1 * bf16_hi(kw[j]));
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1)
+#pragma unroll
+    for (int j = 0; j < kMaxCand; ++j) x[j] += __shfl_xor(x[j], off);
+  float m = kNegInf;
+#pragma unroll
+  for (int j = 0; j < kMaxCand; ++j) {
+    x[j] = j <= i ? x[j] * p.scale_log2 : kNegInf;
+    m = fmaxf(m, x[j]);
+  }
+  // m* over the frontier (finite: every query sees candidate 0) and the slots
+  const float ms_lane = lane < nslot ? m_lane : kNegInf;
+  float mslot = ms_lane;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mslot = fmaxf(mslot, __shfl_xor(mslot, off));
+  m = fmaxf(m, mslot);
+  const float f_lane = exp2_fast(ms_lane - m);    // slot scale in lane s; 0 past the count
+  float lsum = f_lane * l_lane;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) lsum += __shfl_xor(lsum, off);
+  float l = 0.f, a0 = 0.f, a1 = 0.f;
+#pragma unroll
+  for (int j = 0; j < kMaxCand; ++j) {
+    if (j <= i) {
+      const float pj = exp2_fast(x[j] - m);
+      l += pj;
+      a0 = fmaf(pj, bf16_lo(vw[j]), a0);
+      a1 = fmaf(pj, bf16_hi(vw[j]), a1);
+    }
+  }
+  l += lsum;
+#pragma unroll
+  for (int s = 0; s < kNumSlots; ++s) {
+    const float f = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, f_lane), s));
+    a0 = fmaf(f, as[s].x, a0);
+    a1 = fmaf(f, as[s].y, a1);
+  }
+  const float inv = 1.0f / l;
+  reinterpret_cast<float2 *>(p.out + (size_t)row * kHeadDim)[lane] = make_float2(a0 * inv, a1 * inv);
+  if (p.lse != nullptr && lane == 0) p.lse[row] = m * 0.69314718055994531f + logf(l);
 }
 
 }  // namespace
@@ -1199,27 +1114,25 @@ using ChunkSmall = ChunkParamsT<128, 256, 128>;
 using ChunkMedium = ChunkParamsT<512, 1024, 256>;
 using FinalSmall = FinalParamsT<64>;
 
-template <bool Wide, bool Fused, typename D>
+template <bool Wide, typename D>
 hipError_t launch_chunk_as(const ChunkParams &p, hipStream_t s) {
   static thread_local D d;
   static_cast<ChunkHeader &>(d) = p;
   std::memcpy(d.units, p.units, sizeof(uint32_t) * p.num_units);
   std::memcpy(d.wg_first, p.wg_first, sizeof(uint16_t) * (p.num_wgs + 1));
   std::memcpy(d.items, p.items, sizeof(Item) * p.num_items);
-  hipLaunchKernelGGL((chunk_attn<Wide, Fused, D>), dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, d);
+  hipLaunchKernelGGL((chunk_attn<Wide, D>), dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, d);
   return hipGetLastError();
 }
 
-template <bool Wide, bool Fused>
+template <bool Wide>
 hipError_t launch_chunk_sized(const ChunkParams &p, hipStream_t s) {
   auto fits = [&](int units, int items, int wgs) {
     return p.num_units <= units && p.num_items <= items && p.num_wgs <= wgs;
   };
-  if (fits(ChunkSmall::kUnits, ChunkSmall::kItems, ChunkSmall::kWgs))
-    return launch_chunk_as<Wide, Fused, ChunkSmall>(p, s);
-  if (fits(ChunkMedium::kUnits, ChunkMedium::kItems, ChunkMedium::kWgs))
-    return launch_chunk_as<Wide, Fused, ChunkMedium>(p, s);
-  hipLaunchKernelGGL((chunk_attn<Wide, Fused, ChunkParams>), dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, p);
+  if (fits(ChunkSmall::kUnits, ChunkSmall::kItems, ChunkSmall::kWgs)) return launch_chunk_as<Wide, ChunkSmall>(p, s);
+  if (fits(ChunkMedium::kUnits, ChunkMedium::kItems, ChunkMedium::kWgs)) return launch_chunk_as<Wide, ChunkMedium>(p, s);
+  hipLaunchKernelGGL((chunk_attn<Wide, ChunkParams>), dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
@@ -1227,22 +1140,19 @@ hipError_t launch_chunk_sized(const ChunkParams &p, hipStream_t s) {
 
 hipError_t launch_chunk(const ChunkParams &p, hipStream_t s) {
   // a launch with any unit of more than two 16-row blocks runs on the wide kernel
-  bool wide = false;
-  for (int u = 0; u < p.num_units && !wide; ++u) {
-    const uint32_t kind = (p.units[u] >> 17) & 0x7u;
-    wide = kind == kUnitMfma3 || kind == kUnitMfma4;
-  }
-  if (p.done != nullptr) return wide ? launch_chunk_sized<true, true>(p, s) : launch_chunk_sized<false, true>(p, s);
-  return wide ? launch_chunk_sized<true, false>(p, s) : launch_chunk_sized<false, false>(p, s);
+  for (int u = 0; u < p.num_units; ++u)
+    if ((int)(p.units[u] >> 24) >= kUnitMfma3) return launch_chunk_sized<true>(p, s);
+  return launch_chunk_sized<false>(p, s);
 }
 
 hipError_t launch_clear_counters(uint32_t *counters, int n, hipStream_t s) {
-  hipLaunchKernelGGL(clear_counters_kernel, dim3(1), dim3(256), 0, s, counters, n);
+  hipLaunchKernelGGL(clear_counters_kernel, dim3(1), dim3(64), 0, s, counters, n);
   return hipGetLastError();
 }
-
 hipError_t launch_finalize(const FinalParams &p, hipStream_t s) {
-  const dim3 grid(p.Hkv, p.num_items);
+  int rows = 0;
+  for (int i = 0; i < p.num_items; ++i) rows = rows > p.items[i].n_cand * p.Hq ? rows : p.items[i].n_cand * p.Hq;
+  const dim3 grid(p.num_items, (rows + kWaves - 1) / kWaves);
   if (p.num_items <= FinalSmall::kItems) {
     static thread_local FinalSmall d;
     static_cast<FinalHeader &>(d) = p;

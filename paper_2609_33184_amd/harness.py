@@ -57,19 +57,15 @@ def hbm_history(w: Workload, layer: int = 0, device="cuda", kv_layout: int = ss.
 
 def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor]], stream: int,
               order: Optional[Sequence[int]] = None, cand_position: Optional[int] = None,
-              lens: Optional[Sequence[Sequence[int]]] = None, batch: int = 1, fused: bool = False) -> None:
+              lens: Optional[Sequence[Sequence[int]]] = None, batch: int = 1) -> None:
     """Enqueue one whole round (init, history chunks, candidates, finalize)
     on `stream`; results land in b.out / b.lse.  ``batch`` > 1 groups that
-    many consecutive chunks into one ss_attend_history_chunks call.  With
-    ``fused`` the last group of chunks and the finalize go through one
-    ss_round_finalize_chunks call (the candidates are attended before it)."""
+    many consecutive chunks into one ss_attend_history_chunks call."""
     w = b.w
     order = list(range(len(chunks))) if order is None else list(order)
     pos = len(order) if cand_position is None else cand_position
     step = max(1, batch)
     groups = [order[i0:i0 + step] for i0 in range(0, len(order), step)]
-    if fused and groups:
-        pos = min(pos, (len(groups) - 1) * step)   # candidates before the fused last call
     r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream)
 
     def args(grp):
@@ -84,9 +80,6 @@ def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor
             if done <= pos < done + len(grp) or (pos == done and gi == 0):
                 ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
             ks, vs, ls = args(grp)
-            if fused and gi == len(groups) - 1:
-                ss.ss_round_finalize_chunks(r, ks, vs, ls, b.out.data_ptr(), b.lse.data_ptr(), None, None, stream)
-                return
             if batch > 1:
                 ss.ss_attend_history_chunks(r, ks, vs, ls, None, None, stream)
             else:
@@ -100,7 +93,7 @@ def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor
 
 
 def capture_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor]], batch: int = 1,
-                  pool=None, fused: bool = False) -> "torch.cuda.CUDAGraph":
+                  pool=None) -> "torch.cuda.CUDAGraph":
     """Capture one whole round (the same calls as run_round) into a HIP graph.
 
     Every step the library enqueues is a kernel launch with its arguments by
@@ -112,7 +105,7 @@ def capture_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Te
     g = torch.cuda.CUDAGraph()
     torch.cuda.synchronize()
     with torch.cuda.graph(g, pool=pool):
-        run_round(b, chunks, torch.cuda.current_stream().cuda_stream, batch=batch, fused=fused)
+        run_round(b, chunks, torch.cuda.current_stream().cuda_stream, batch=batch)
     return g
 
 
@@ -211,8 +204,8 @@ def run_round_restored(b: RoundBuffers, host: HostHistory, dev: Sequence[torch.T
                        stream: int) -> None:
     """Restore, then attend: every chunk of the history goes to its own
     device buffer (``dev[j]``, at least host.sizes[j] bytes) on the copy
-    stream, and one batched call, fused with finalize, attends all of them
-    once the last upload is done."""
+    stream, and one batched call attends all of them once the last upload is
+    done."""
     w = b.w
     n = w.num_chunks
     done = ss.ss_event_create()
@@ -224,11 +217,12 @@ def run_round_restored(b: RoundBuffers, host: HostHistory, dev: Sequence[torch.T
                                    done if j == last else None)
         r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream)
         try:
-            ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
             ks = [dev[j].data_ptr() for j in range(n)]
             vs = [dev[j].data_ptr() + _chunk_vofs(w, host, j, b.kv_layout) for j in range(n)]
-            ss.ss_round_finalize_chunks(r, ks, vs, [w.chunk_lens(j) for j in range(n)], b.out.data_ptr(),
-                                        b.lse.data_ptr(), done if last >= 0 else None, None, stream)
+            ss.ss_attend_history_chunks(r, ks, vs, [w.chunk_lens(j) for j in range(n)],
+                                        done if last >= 0 else None, None, stream)
+            ss.ss_attend_local_candidates(r, b.kc.data_ptr(), b.vc.data_ptr(), stream)
+            ss.ss_round_finalize(r, b.out.data_ptr(), b.lse.data_ptr(), stream)
         finally:
             ss.ss_round_destroy(r)
     finally:

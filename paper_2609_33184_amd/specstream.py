@@ -32,7 +32,7 @@ SS_KV_HEAD_MAJOR_KV = 2  # history chunk [Hkv][sum len][2][d]: K and V rows of a
 EXPORTED = (
     "ss_round_workspace_bytes", "ss_round_init", "ss_upload_chunk", "ss_attend_history_chunk",
     "ss_attend_history_chunks",
-    "ss_attend_local_candidates", "ss_round_finalize", "ss_round_finalize_chunks",
+    "ss_attend_local_candidates", "ss_round_finalize",
     "ss_round_destroy", "ss_pipeline_create",
     "ss_pipeline_attend_chunk", "ss_pipeline_attend_chunks", "ss_pipeline_destroy", "ss_event_create", "ss_event_destroy",
     "ss_status_string", "ss_last_error",
@@ -103,7 +103,6 @@ def load() -> ctypes.CDLL:
         "ss_attend_history_chunks": (I32, [P, I32, ctypes.POINTER(P), ctypes.POINTER(P), PI32, P, P, P]),
         "ss_attend_local_candidates": (I32, [P, P, P, P]),
         "ss_round_finalize": (I32, [P, P, P, P]),
-        "ss_round_finalize_chunks": (I32, [P, I32, ctypes.POINTER(P), ctypes.POINTER(P), PI32, P, P, P, P, P]),
         "ss_round_destroy": (None, [P]),
         "ss_pipeline_create": (I32, [ctypes.POINTER(P), P, P, SZ, P]),
         "ss_pipeline_attend_chunk": (I32, [P, P, P, PI32, P]),
@@ -196,17 +195,6 @@ def ss_attend_local_candidates(r: int, k_cand: int, v_cand: int, stream: int = 0
 
 def ss_round_finalize(r: int, out: int, lse: Optional[int] = None, stream: int = 0) -> None:
     _check(load().ss_round_finalize(r, out, lse, stream), "ss_round_finalize")
-
-
-def ss_round_finalize_chunks(r: int, k: Sequence[int], v: Sequence[int], lens: Sequence[Sequence[int]],
-                             out: int, lse: Optional[int] = None, wait_before: Optional[int] = None,
-                             signal_after: Optional[int] = None, stream: int = 0) -> None:
-    n = len(k)
-    kp = (ctypes.c_void_p * n)(*k)
-    vp = (ctypes.c_void_p * n)(*v)
-    flat = [int(x) for row in lens for x in row]
-    _check(load().ss_round_finalize_chunks(r, n, kp, vp, (ctypes.c_int32 * len(flat))(*flat), wait_before,
-                                           signal_after, out, lse, stream), "ss_round_finalize_chunks")
 
 
 def ss_round_destroy(r: Optional[int]) -> None:

@@ -105,9 +105,6 @@ void expect_failed(ss_round *r, Shape &s, const char *what) {
   CHECK(history(r, s) == SS_ERR_BAD_STATE, "%s: history after failure", what);
   CHECK(ss_attend_local_candidates(r, KC, VC, nullptr) == SS_ERR_BAD_STATE, "%s: candidates after failure", what);
   CHECK(ss_round_finalize(r, OUT, nullptr, nullptr) == SS_ERR_BAD_STATE, "%s: finalize after failure", what);
-  const void *k = (const void *)0x200000000000ull, *v = (const void *)0x300000000000ull;
-  CHECK(ss_round_finalize_chunks(r, 1, &k, &v, s.lens.data(), nullptr, nullptr, OUT, nullptr, nullptr) ==
-            SS_ERR_BAD_STATE, "%s: fused finalize after failure", what);
   CHECK(g_launches == 0 && g_hip_calls == 0, "%s: a refused call enqueued work", what);
 }
 
@@ -171,18 +168,6 @@ int main() {
     arm(0, -1);
     CHECK(ss_round_finalize(r, OUT, nullptr, nullptr) == SS_ERR_HIP, "finalize failure not reported");
     expect_failed(r, s, "finalize launch");
-    ss_round_destroy(r);
-  }
-  {  // the fused launch fails
-    Shape s = tailed();
-    ss_round *r = init(s, d);
-    arm(-1, -1);
-    CHECK(ss_attend_local_candidates(r, KC, VC, nullptr) == SS_OK, "setup");
-    arm(1, -1);   // launch 0 is the counter clear
-    const void *k = (const void *)0x200000000000ull, *v = (const void *)0x300000000000ull;
-    CHECK(ss_round_finalize_chunks(r, 1, &k, &v, s.lens.data(), nullptr, nullptr, OUT, nullptr, nullptr) == SS_ERR_HIP,
-          "fused launch failure not reported");
-    expect_failed(r, s, "fused launch");
     ss_round_destroy(r);
   }
   {  // host allocation failures: init, a history call, pipeline creation

@@ -7,9 +7,6 @@
 // emulated with the workgroups interleaved at random, from a zero counter
 // (every (tail unit, KV head) pair claimed once, the counter left at zero)
 // and from counters that are not zero (no claim outside the tail's range).
-// Fused finalize launches are checked for their per-request finalize items:
-// each request's unit count, slot count and a finalize-only unit for a
-// request without tokens, and the done-counter protocol is emulated.
 // The kernel launchers are stubs that record the launch tables.
 #include "ss_kernels.h"
 #include "specstream.h"
@@ -25,7 +22,7 @@
 namespace {
 struct Rec {
   std::vector<ss::Item> items; std::vector<uint32_t> units; std::vector<uint16_t> wg_first; int kind;
-  int tail_first, num_tail; uint32_t *claim; int clears_before; uint32_t *done; int fin_first; int Hkv;
+  int tail_first, num_tail; uint32_t *claim; int clears_before; int Hkv;
 };
 int g_finalize_launches = 0;
 int g_clear_n = 0;
@@ -44,7 +41,7 @@ static void rec(const ChunkParams &p, int kind) {
   if (p.num_wgs < 1 || p.num_wgs > kMaxWgs) { printf("bad workgroup count\n"); exit(1); }
   r.kind = kind;
   r.tail_first = p.tail_first; r.num_tail = p.num_tail; r.claim = p.claim; r.clears_before = g_clears;
-  r.done = p.done; r.fin_first = p.fin_first; r.Hkv = p.Hkv;
+  r.Hkv = p.Hkv;
   if (p.num_units < 1 || p.num_units > kMaxUnits || p.num_items < 1 || p.num_items > kMaxItems) { printf("bad counts\n"); exit(1); }
   g_recs.push_back(r);
   g_last = &p;
@@ -67,10 +64,8 @@ static int tiles_of(const ss::Item &it) { return (it.tok_count + ss::kTile - 1) 
 static int fails = 0;
 #define CHECK(c, ...) do { if (!(c)) { printf("FAIL %s:%d: ", __FILE__, __LINE__); printf(__VA_ARGS__); printf("\n"); if (++fails > 20) exit(1); } } while (0)
 
-struct UnitF { int i0, nit, kind, req; };
-static UnitF unit_fields(uint32_t u) {
-  return UnitF{(int)(u & 0xfff), (int)((u >> 12) & 0x1f), (int)((u >> 17) & 0x7), (int)(u >> 20)};
-}
+struct UnitF { int i0, nit, kind; };
+static UnitF unit_fields(uint32_t u) { return UnitF{(int)(u & 0xffff), (int)((u >> 16) & 0xff), (int)(u >> 24)}; }
 
 // The history kernel's claim loop, with the launch's workgroups interleaved
 // at random: a workgroup claims only after its own units, makes claims until
@@ -98,10 +93,9 @@ static std::vector<std::pair<int, int>> emulate_claims(const Rec &rc, uint32_t s
   return got;
 }
 
-// emulate one history call (fused: the round's last call, with finalize)
+// emulate one history call
 static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, const std::vector<std::vector<int>> &lens,
-                       int split, int layout, int mfma_min_rows, std::vector<int> &slots_used, ss_round *r,
-                       bool fused = false) {
+                       int split, int layout, int mfma_min_rows, std::vector<int> &slots_used, ss_round *r) {
   const int nch = (int)lens.size();
   std::vector<int32_t> flat;
   std::vector<long> tot(nch, 0);
@@ -114,27 +108,11 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
   }
   g_recs.clear();
   g_finalize_launches = 0;
-  ss_status s;
-  if (fused) {
-    s = ss_attend_local_candidates(r, (const void *)0x7f2000000000ull, (const void *)0x7f3000000000ull, nullptr);
-    CHECK(s == SS_OK, "candidates status %d: %s", s, ss_last_error());
-    s = ss_round_finalize_chunks(r, nch, kp.data(), vp.data(), flat.data(), nullptr, nullptr,
-                                 (float *)0x7f4000000000ull, (float *)0x7f5000000000ull, nullptr);
-  } else {
-    s = ss_attend_history_chunks(r, nch, kp.data(), vp.data(), flat.data(), nullptr, nullptr, nullptr);
-  }
+  const ss_status s = ss_attend_history_chunks(r, nch, kp.data(), vp.data(), flat.data(), nullptr, nullptr, nullptr);
   CHECK(s == SS_OK, "status %d: %s", s, ss_last_error());
   if (s != SS_OK) return;
   long total = 0;
   for (auto &row : lens) for (int x : row) total += x;
-  if (fused) {
-    // one fused launch, or (did not fit) history launches and the finalize kernel
-    const bool one = g_recs.size() == 1 && g_recs[0].done != nullptr;
-    CHECK(one || g_finalize_launches == 1, "fused call: %zu launches, %d finalize launches", g_recs.size(),
-          g_finalize_launches);
-    CHECK(!one || g_finalize_launches == 0, "fused launch and a finalize launch");
-    CHECK(total > 0 || !one, "fused launch without tokens");
-  }
   // coverage[b][c] token counts
   std::vector<std::vector<std::vector<int>>> cov(B, std::vector<std::vector<int>>(nch));
   for (int b = 0; b < B; ++b) for (int c = 0; c < nch; ++c) cov[b][c].assign(lens[c][b], 0);
@@ -161,14 +139,14 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
   // counter block: at the workspace's end, cleared once per round (before
   // the first launch that uses it) unless the caller said it is zero
   const size_t ws_end = 0x7f1000000000ull + ss_round_workspace_bytes(g_desc);
-  const size_t block_words = ss::kClaimCounters + (size_t)B * Hkv;
+  const size_t block_words = ss::kClaimCounters;
   const uintptr_t block = ws_end - (block_words * 4 + 255) / 256 * 256;
   for (auto &rc : g_recs) {
-    if (rc.num_tail == 0 && rc.done == nullptr) {
+    if (rc.num_tail == 0) {
       CHECK(rc.wg_first.back() == rc.units.size(), "units beyond the workgroup lists");
       continue;
     }
-    CHECK(g_recs.size() == 1, "a call with a tail or fused finalize took %zu launches", g_recs.size());
+    CHECK(g_recs.size() == 1, "a call with a tail took %zu launches", g_recs.size());
     if (g_desc->counters_zeroed) {
       CHECK(g_clears == 0, "counters cleared although the caller said they are zero");
     } else {
@@ -198,50 +176,12 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
                 "claim from counter %u outside the tail: unit %d head %d", start, pr.first, pr.second);
       }
     }
-    if (rc.done != nullptr) {
-      CHECK((uintptr_t)rc.done == block + 4 * ss::kClaimCounters, "done counters not after the claim words");
-      CHECK(rc.fin_first >= 0 && rc.fin_first + B == (int)rc.items.size(), "finalize items at the table's end");
-      // per request: units in the launch and the finalize item
-      std::vector<int> units(B, 0), final_only(B, 0);
-      for (size_t u = 0; u < rc.units.size(); ++u) {
-        const UnitF f = unit_fields(rc.units[u]);
-        CHECK(f.req >= 0 && f.req < B, "unit request");
-        if (f.req < 0 || f.req >= B) continue;
-        ++units[f.req];
-        if (f.kind == ss::kUnitFinal) {
-          ++final_only[f.req];
-          CHECK(f.nit == 0 && (int)u < rc.tail_first + (rc.num_tail ? 0 : (int)rc.units.size()), "finalize-only unit");
-        } else {
-          CHECK(rc.items[f.i0].q_row0 == off_rows[f.req], "unit request %d does not match its items", f.req);
-        }
-      }
-      for (int b = 0; b < B; ++b) {
-        const ss::Item &fi = rc.items[rc.fin_first + b];
-        long toks = 0;
-        for (auto &row : lens) toks += row[b];
-        CHECK(fi.q_row0 == off_rows[b] && fi.n_cand == ncand[b], "finalize item %d", b);
-        CHECK(fi.slot == units[b] && units[b] >= 1, "request %d: %d units, finalize item says %d", b, units[b], fi.slot);
-        CHECK((toks == 0) == (final_only[b] == 1) && final_only[b] <= 1, "request %d: %d finalize-only units, %ld tokens",
-              b, final_only[b], toks);
-        // every unit of (b, g) counts once; the count's last unit finalizes and leaves the counter zero
-        for (int g = 0; g < Hkv; ++g) {
-          uint32_t ctr = 0;
-          int finals = 0;
-          for (int k = 0; k < units[b]; ++k) {
-            const uint32_t c = ctr++;
-            if (c + 1u == (uint32_t)fi.slot) { ctr = 0; ++finals; }
-          }
-          CHECK(finals == 1 && ctr == 0, "request %d head %d: %d finalizes, counter %u", b, g, finals, ctr);
-        }
-      }
-    }
   }
   for (auto &rc : g_recs) {
     for (size_t u = 0; u < rc.units.size(); ++u) {
       const UnitF f = unit_fields(rc.units[u]);
       const int i0 = f.i0, nit = f.nit, kind = f.kind;
-      if (kind == ss::kUnitFinal) continue;
-      CHECK(nit >= 1 && nit <= ss::kMaxChain && i0 + nit <= (rc.done ? rc.fin_first : (int)rc.items.size()), "unit table");
+      CHECK(nit >= 1 && nit <= ss::kMaxChain && i0 + nit <= (int)rc.items.size(), "unit table");
       const ss::Item &it = rc.items[i0];
       int b = -1;
       for (int bb = 0; bb < B; ++bb) if (off_rows[bb] == it.q_row0) b = bb;
@@ -310,9 +250,9 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
   }
 }
 
-// One round of history calls in batches of `batch` chunks, planned three
-// ways: separate calls then finalize; the last batch fused with finalize;
-// the same with a workspace the caller declared zeroed.
+// One round of history calls in batches of `batch` chunks, then the
+// finalize, on a workspace of unknown contents and on one the caller
+// declared zeroed.
 static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> ncand, std::vector<int> hist, int S,
                      int split, int layout, int batch, int mfma_min_rows = 0, int balance = 0, int expect_tail = -1,
                      int expect_wgs = -1) {
@@ -320,13 +260,12 @@ static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> 
   std::vector<std::vector<int>> lens(nch, std::vector<int>(B));
   long maxc = 1;
   for (int c = 0; c < nch; ++c) { long t = 0; for (int b = 0; b < B; ++b) { lens[c][b] = std::max(0, std::min(S, hist[b] - c * S)); t += lens[c][b]; } maxc = std::max(maxc, t); }
-  for (int mode = 0; mode < 3; ++mode) {
-    const bool fused = mode > 0;
+  for (int mode = 0; mode < 2; ++mode) {
     ss_round_desc d{};
     d.num_requests = B; d.num_q_heads = Hq; d.num_kv_heads = Hkv; d.head_dim = 128; d.softmax_scale = 0.088f;
     d.num_cand = ncand.data(); d.max_chunk_tokens = (int)maxc; d.split_tokens = split; d.mfma_min_rows = mfma_min_rows; d.kv_layout = layout;
     d.balance_permille = balance;
-    d.counters_zeroed = mode == 2;
+    d.counters_zeroed = mode == 1;
     g_desc = &d; g_clears = 0; g_clear_ptr = nullptr; g_tail_calls = 0;
     ss_round *r = nullptr;
     size_t ws = ss_round_workspace_bytes(&d);
@@ -334,31 +273,26 @@ static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> 
     if (s != SS_OK) { printf("%s: init failed %s\n", name, ss_last_error()); fails++; return; }
     std::vector<int> used(B, 0);
     const int before = fails;
-    bool fused_launch = false;
     // chunk batches
     for (int c0 = 0; c0 < nch; c0 += batch) {
       std::vector<std::vector<int>> part(lens.begin() + c0, lens.begin() + std::min(nch, c0 + batch));
-      const bool last = c0 + batch >= nch;
-      check_call(B, Hq, Hkv, ncand, part, split, layout, mfma_min_rows, used, r, fused && last);
-      if (fused && last) fused_launch = g_recs.size() == 1 && g_recs[0].done != nullptr;
+      check_call(B, Hq, Hkv, ncand, part, split, layout, mfma_min_rows, used, r);
     }
-    if (!fused) {
-      s = ss_attend_local_candidates(r, (const void *)0x7f2000000000ull, (const void *)0x7f3000000000ull, nullptr);
-      if (s == SS_OK) s = ss_round_finalize(r, (float *)0x7f4000000000ull, nullptr, nullptr);
-      CHECK(s == SS_OK, "finalize: %s", ss_last_error());
-    }
+    g_finalize_launches = 0;
+    s = ss_attend_local_candidates(r, (const void *)0x7f2000000000ull, (const void *)0x7f3000000000ull, nullptr);
+    if (s == SS_OK) s = ss_round_finalize(r, (float *)0x7f4000000000ull, nullptr, nullptr);
+    CHECK(s == SS_OK && g_finalize_launches == 1, "finalize: %s", ss_last_error());
     ss_round_destroy(r);
-    const int want_clears = mode == 2 ? 0 : (g_tail_calls > 0 || fused_launch) ? 1 : 0;
-    CHECK(g_clears == want_clears, "%d clears for %d balanced calls (fused launch %d)", g_clears, g_tail_calls,
-          (int)fused_launch);
+    const int want_clears = mode == 1 ? 0 : g_tail_calls > 0 ? 1 : 0;
+    CHECK(g_clears == want_clears, "%d clears for %d balanced calls", g_clears, g_tail_calls);
     if (expect_tail >= 0) CHECK((g_tail_calls > 0) == (expect_tail > 0), "%s: %d balanced calls", name, g_tail_calls);
     // workgroups per KV head of the last call's launches
     if (expect_wgs >= 0)
       for (auto &rc : g_recs)
         CHECK((int)rc.wg_first.size() - 1 == expect_wgs, "%s: %d workgroups per KV head, want %d", name,
               (int)rc.wg_first.size() - 1, expect_wgs);
-    printf("%-44s %-14s %s (launches in last call: %zu, balanced calls: %d)\n", name,
-           mode == 0 ? "separate" : mode == 1 ? (fused_launch ? "fused" : "fused(2 calls)") : "fused, zeroed",
+    printf("%-44s %-7s %s (launches in last call: %zu, balanced calls: %d)\n", name,
+           mode == 0 ? "" : "zeroed",
            fails == before ? "ok" : "FAILED", g_recs.size(), g_tail_calls);
   }
 }

@@ -62,8 +62,7 @@ def _ws(cands, hq, hkv):
     rows = sum(cands) * hq
     a = -(-32 * rows * 128 * 4 // 256) * 256     # 32 state slots per row
     m = -(-32 * rows * 4 // 256) * 256
-    counters = -(-(64 + len(cands) * hkv) * 4 // 256) * 256   # claim words, then one per (request, KV head)
-    return a + 2 * m + counters
+    return a + 2 * m + 256                        # + the counter block (the tail's claim counter)
 
 
 def test_workspace_bytes_and_descriptor_validation(lib):
@@ -129,7 +128,6 @@ def test_call_order_and_chunk_arguments(lib):
             assert e.value.status == status, e.value
 
         expect(ss.SS_ERR_BAD_STATE, ss.ss_round_finalize, r, FAKE_Q, 0)            # before candidates
-        expect(ss.SS_ERR_BAD_STATE, ss.ss_round_finalize_chunks, r, [K], [V], [[10, 3]], FAKE_Q)
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_history_chunk, r, K, V, [600, 600])   # > max_chunk_tokens
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_history_chunk, r, K, V, [-1, 3])
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_attend_history_chunk, r, K + 2, V, [10, 3])  # misaligned
@@ -148,8 +146,6 @@ def test_call_order_and_chunk_arguments(lib):
         expect(ss.SS_ERR_BAD_STATE, ss.ss_attend_local_candidates, r, K, V)
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_round_finalize, r, 0, 0)          # null out
         expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_round_finalize, r, FAKE_Q + 4, 0)  # misaligned out
-        expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_round_finalize_chunks, r, [K], [V], [[10, 3]], 0)
-        expect(ss.SS_ERR_INVALID_ARGUMENT, ss.ss_round_finalize_chunks, r, [K], [V], [[600, 600]], FAKE_Q)
     finally:
         ss.ss_round_destroy(r)
     ss.ss_round_destroy(None)
