@@ -30,7 +30,8 @@
  *     multiplies the dot product (1/sqrt(d) in the paper, Sec. 4.2).
  *   - Ownership: the caller owns every buffer, stream and event and keeps
  *     them alive until the enqueued work has finished.  The library never
- *     allocates device memory; its only state is the host handles.
+ *     allocates device memory at run time; its state is the host handles
+ *     and the static device scratch that ss_round_init_scratch uses.
  *   - Asynchrony: calls validate, enqueue on the given stream and return.
  *     A non-OK status means nothing was enqueued by that call, except
  *     SS_ERR_HIP, reported when a HIP call itself fails: if part of the
@@ -337,6 +338,24 @@ int32_t ss_width_select(ss_width_ctl *c);
 /* The controller's estimate of seconds per committed token at `width` (-1
  * for an unknown width). */
 double ss_width_estimate(const ss_width_ctl *c, int32_t width);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): start a
+ * round as ss_round_init does, but with the library's own device scratch as
+ * its workspace instead of a caller buffer, so no device memory is allocated
+ * and no workspace argument is needed.  The scratch is a 64 MiB device array
+ * per GPU (ss_round_workspace_bytes(desc) must not exceed it, else
+ * SS_ERR_WORKSPACE), held from the library's first use on that GPU until the
+ * process ends; its address is looked up on the calling thread's current
+ * device at the first call there.  Every round started this way on one GPU
+ * shares that scratch, which keeps the previous round's contents: rounds
+ * whose work overlaps on one GPU (other streams, or a round started before
+ * the previous one's work completed without a stream order between them)
+ * race.  desc->counters_zeroed is ignored: the counter block's place in the
+ * scratch depends on the round's size, so the round's first history call
+ * with a balancing tail always clears it.  Every other call of the round is
+ * the ordinary one; the host handle is freed with ss_round_destroy. */
+ss_status ss_round_init_scratch(ss_round **out, const ss_round_desc *desc, const void *q, hipStream_t stream);
 
 /* Event helpers so callers need no HIP binding of their own.  Events are
  * created with timing disabled. */

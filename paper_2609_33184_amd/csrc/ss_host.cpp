@@ -820,6 +820,25 @@ ss_status ss_round_finalize(ss_round *r, float *out, float *lse, hipStream_t str
   });
 }
 
+ss_status ss_round_init_scratch(ss_round **out, const ss_round_desc *desc, const void *q, hipStream_t stream) {
+  (void)stream;
+  if (out == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "out is null");
+  *out = nullptr;
+  const size_t need = ss_round_workspace_bytes(desc);
+  if (need == 0) return validate_desc(desc);   // sets the detail
+  if (need > ss::kScratchBytes)
+    return fail(SS_ERR_WORKSPACE, "the round needs %zu bytes of workspace; the library's scratch holds %zu",
+                need, ss::kScratchBytes);
+  void *scratch = nullptr;
+  const hipError_t e = ss::scratch_address(&scratch);
+  if (e != hipSuccess) return hip_fail(e, "scratch address lookup");
+  const ss_status st = init_round(out, desc, q, scratch, ss::kScratchBytes);
+  // The counter block sits at the end of this round's share of the scratch,
+  // where an earlier round of another size may have left state: always clear.
+  if (st == SS_OK) (*out)->counters_ready = false;
+  return st;
+}
+
 void ss_round_destroy(ss_round *r) { delete r; }
 
 ss_status ss_pipeline_create(ss_pipeline **out, void *staging0, void *staging1, size_t slot_bytes,

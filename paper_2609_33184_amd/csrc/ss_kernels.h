@@ -133,4 +133,11 @@ hipError_t launch_finalize(const FinalParams &p, hipStream_t s);
 // captured in a graph).
 hipError_t launch_clear_counters(uint32_t *counters, int n, hipStream_t s);
 
+// The library's own device scratch: a file-scope device array of
+// kScratchBytes that serves as the workspace of rounds started with
+// ss_round_init_scratch.  scratch_address returns its address on the
+// current device (looked up once per device, then cached).
+constexpr size_t kScratchBytes = size_t(64) << 20;
+hipError_t scratch_address(void **ptr);
+
 }  // namespace ss

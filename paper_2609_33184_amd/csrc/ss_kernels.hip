@@ -26,6 +26,7 @@
 
 #include <math.h>
 
+#include <mutex>
 #include <type_traits>
 
 namespace ss {
@@ -43,6 +44,7 @@ constexpr int kBufferFlags = 0x00020000;   // buffer resource word 3: 32-bit dat
 // reusable lines; measured on MI355X, this took config 3's round from 378 to
 // 354 us and config 4's from 786 to 743 us (means over 40 rounds).
 constexpr int kStreamLoad = 2;
+constexpr int kMaxDevices = 64;   // devices whose scratch address is cached
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -1103,6 +1105,10 @@ __global__ void __launch_bounds__(256) finalize_kernel(const P p) {
   if (p.lse != nullptr && lane == 0) p.lse[row] = m * 0.69314718055994531f + logf(l);
 }
 
+// The library's device scratch (see scratch_address).  Each GPU the library
+// runs on holds its own copy until the process ends.
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 }  // namespace
 
 namespace {
@@ -1162,6 +1168,27 @@ hipError_t launch_finalize(const FinalParams &p, hipStream_t s) {
     hipLaunchKernelGGL(finalize_kernel<FinalParams>, grid, dim3(256), 0, s, p);
   }
   return hipGetLastError();
+}
+
+hipError_t scratch_address(void **ptr) {
+  // One lookup per device, with that device current; the array's name is a
+  // host-side stand-in, so only the looked-up address may reach a kernel.
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void *a = nullptr;
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (a == nullptr) return hipErrorInvalidSymbol;
+    addr[dev] = a;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace ss

@@ -57,16 +57,21 @@ def hbm_history(w: Workload, layer: int = 0, device="cuda", kv_layout: int = ss.
 
 def run_round(b: RoundBuffers, chunks: Sequence[Tuple[torch.Tensor, torch.Tensor]], stream: int,
               order: Optional[Sequence[int]] = None, cand_position: Optional[int] = None,
-              lens: Optional[Sequence[Sequence[int]]] = None, batch: int = 1) -> None:
+              lens: Optional[Sequence[Sequence[int]]] = None, batch: int = 1, scratch: bool = False) -> None:
     """Enqueue one whole round (init, history chunks, candidates, finalize)
     on `stream`; results land in b.out / b.lse.  ``batch`` > 1 groups that
-    many consecutive chunks into one ss_attend_history_chunks call."""
+    many consecutive chunks into one ss_attend_history_chunks call.  With
+    ``scratch`` the round starts with ss_round_init_scratch (the
+    library's own workspace) instead of b.ws."""
     w = b.w
     order = list(range(len(chunks))) if order is None else list(order)
     pos = len(order) if cand_position is None else cand_position
     step = max(1, batch)
     groups = [order[i0:i0 + step] for i0 in range(0, len(order), step)]
-    r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream)
+    if scratch:
+        r = ss.ss_round_init_scratch(b.desc, b.q.data_ptr(), stream)
+    else:
+        r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream)
 
     def args(grp):
         ks = [chunks[j][0].data_ptr() if chunks[j][0].numel() else 0 for j in grp]

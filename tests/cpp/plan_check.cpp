@@ -52,10 +52,12 @@ hipError_t launch_finalize(const FinalParams &, hipStream_t) { ++g_finalize_laun
 hipError_t launch_clear_counters(uint32_t *c, int n, hipStream_t) {
   ++g_clears; g_clear_ptr = c; g_clear_n = n; return hipSuccess;
 }
-
+// The scratch stands at the same address as the caller workspaces below.
+hipError_t scratch_address(void **p) { *p = (void *)0x7f1000000000ull; return hipSuccess; }
 }
 
 static const ss_round_desc *g_desc = nullptr;
+static bool g_trust_zeroed = false;   // the round may skip the counter clear
 static int g_tail_calls = 0;
 static std::mt19937 g_emu(11);
 
@@ -147,7 +149,7 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
       continue;
     }
     CHECK(g_recs.size() == 1, "a call with a tail took %zu launches", g_recs.size());
-    if (g_desc->counters_zeroed) {
+    if (g_trust_zeroed) {
       CHECK(g_clears == 0, "counters cleared although the caller said they are zero");
     } else {
       CHECK(rc.clears_before == 1 && (uintptr_t)g_clear_ptr == block && g_clear_n == (int)block_words,
@@ -251,8 +253,9 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
 }
 
 // One round of history calls in batches of `batch` chunks, then the
-// finalize, on a workspace of unknown contents and on one the caller
-// declared zeroed.
+// finalize, on a workspace of unknown contents, on one the caller declared
+// zeroed, and (when it fits) on the library's scratch with counters_zeroed
+// set, which the scratch round must ignore.
 static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> ncand, std::vector<int> hist, int S,
                      int split, int layout, int batch, int mfma_min_rows = 0, int balance = 0, int expect_tail = -1,
                      int expect_wgs = -1) {
@@ -260,16 +263,23 @@ static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> 
   std::vector<std::vector<int>> lens(nch, std::vector<int>(B));
   long maxc = 1;
   for (int c = 0; c < nch; ++c) { long t = 0; for (int b = 0; b < B; ++b) { lens[c][b] = std::max(0, std::min(S, hist[b] - c * S)); t += lens[c][b]; } maxc = std::max(maxc, t); }
-  for (int mode = 0; mode < 2; ++mode) {
+  for (int mode = 0; mode < 3; ++mode) {
     ss_round_desc d{};
     d.num_requests = B; d.num_q_heads = Hq; d.num_kv_heads = Hkv; d.head_dim = 128; d.softmax_scale = 0.088f;
     d.num_cand = ncand.data(); d.max_chunk_tokens = (int)maxc; d.split_tokens = split; d.mfma_min_rows = mfma_min_rows; d.kv_layout = layout;
     d.balance_permille = balance;
-    d.counters_zeroed = mode == 1;
+    d.counters_zeroed = mode >= 1;
+    g_trust_zeroed = mode == 1;
     g_desc = &d; g_clears = 0; g_clear_ptr = nullptr; g_tail_calls = 0;
     ss_round *r = nullptr;
     size_t ws = ss_round_workspace_bytes(&d);
-    ss_status s = ss_round_init(&r, &d, (const void *)0x7f0000000000ull, (void *)0x7f1000000000ull, ws, nullptr);
+    if (mode == 2 && ws > ss::kScratchBytes) {
+      CHECK(ss_round_init_scratch(&r, &d, (const void *)0x7f0000000000ull, nullptr) == SS_ERR_WORKSPACE && r == nullptr,
+            "%s: a round beyond the scratch was accepted", name);
+      continue;
+    }
+    ss_status s = mode == 2 ? ss_round_init_scratch(&r, &d, (const void *)0x7f0000000000ull, nullptr)
+                            : ss_round_init(&r, &d, (const void *)0x7f0000000000ull, (void *)0x7f1000000000ull, ws, nullptr);
     if (s != SS_OK) { printf("%s: init failed %s\n", name, ss_last_error()); fails++; return; }
     std::vector<int> used(B, 0);
     const int before = fails;
@@ -283,7 +293,7 @@ static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> 
     if (s == SS_OK) s = ss_round_finalize(r, (float *)0x7f4000000000ull, nullptr, nullptr);
     CHECK(s == SS_OK && g_finalize_launches == 1, "finalize: %s", ss_last_error());
     ss_round_destroy(r);
-    const int want_clears = mode == 1 ? 0 : g_tail_calls > 0 ? 1 : 0;
+    const int want_clears = g_trust_zeroed ? 0 : g_tail_calls > 0 ? 1 : 0;
     CHECK(g_clears == want_clears, "%d clears for %d balanced calls", g_clears, g_tail_calls);
     if (expect_tail >= 0) CHECK((g_tail_calls > 0) == (expect_tail > 0), "%s: %d balanced calls", name, g_tail_calls);
     // workgroups per KV head of the last call's launches
@@ -292,7 +302,7 @@ static void scenario(const char *name, int B, int Hq, int Hkv, std::vector<int> 
         CHECK((int)rc.wg_first.size() - 1 == expect_wgs, "%s: %d workgroups per KV head, want %d", name,
               (int)rc.wg_first.size() - 1, expect_wgs);
     printf("%-44s %-7s %s (launches in last call: %zu, balanced calls: %d)\n", name,
-           mode == 0 ? "" : "zeroed",
+           mode == 0 ? "" : mode == 1 ? "zeroed" : "scratch",
            fails == before ? "ok" : "FAILED", g_recs.size(), g_tail_calls);
   }
 }

@@ -175,3 +175,15 @@ def test_upload_argument_checks(lib):
         ss.ss_upload_chunk(FAKE_WS, FAKE_Q, 0)
     assert e.value.status == ss.SS_ERR_INVALID_ARGUMENT
 
+
+def test_scratch_round_rejects_rounds_beyond_the_scratch(lib):
+    """The no-allocation round start checks the workspace a round needs
+    against the library's 64 MiB scratch before it touches a device."""
+    big = ss.make_desc([8] * 64, 32, 8)          # 16384 rows: about 273 MB of slot states
+    assert ss.ss_round_workspace_bytes(big) > 64 << 20
+    with pytest.raises(ss.SpecStreamError) as e:
+        ss.ss_round_init_scratch(big, FAKE_Q)
+    assert e.value.status == ss.SS_ERR_WORKSPACE and "scratch" in str(e.value)
+    with pytest.raises(ss.SpecStreamError) as e:
+        ss.ss_round_init_scratch(ss.make_desc([0], 8, 2), FAKE_Q)
+    assert e.value.status == ss.SS_ERR_INVALID_ARGUMENT
