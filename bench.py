@@ -127,6 +127,39 @@ def copy_probe(torch, stream, nbytes: int = 1 << 31, reps: int = 5):
             "best_GBs_read_plus_written": round(2 * nbytes / t[0] / 1e9, 1)}
 
 
+def read_probe(torch, ss, stream, nbytes: int = 1 << 31, reps: int = 7, grids=(256, 512, 1024, 2048, 4096),
+               settle: int = 100):
+    """Read ceiling: ss_probe_read streams `nbytes` of HBM with the history
+    kernel's load form (16 B per lane, non-temporal, 8 loads in flight per
+    lane) and nothing else, over each grid size, after `settle` untimed
+    reads; GB/s of the best grid's median (HIP events on `stream`)."""
+    buf = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(max(grids), dtype=torch.int32, device="cuda")
+    res = {}
+    with torch.cuda.stream(stream):
+        # the GPU streams slower for its first tens of ms after a pause (see transient_blocks): settle first
+        for _ in range(settle):
+            ss.ss_probe_read(buf.data_ptr(), nbytes, sink.data_ptr(), grids[0], stream.cuda_stream)
+        for g in grids:
+            for _ in range(3):
+                ss.ss_probe_read(buf.data_ptr(), nbytes, sink.data_ptr(), g, stream.cuda_stream)
+            ts = []
+            for _ in range(reps):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                ss.ss_probe_read(buf.data_ptr(), nbytes, sink.data_ptr(), g, stream.cuda_stream)
+                e1.record(stream)
+                ts.append((e0, e1))
+            torch.cuda.synchronize()
+            t = sorted(e0.elapsed_time(e1) / 1e3 for e0, e1 in ts)
+            res[str(g)] = round(nbytes / t[len(t) // 2] / 1e9, 1)
+    del buf, sink
+    torch.cuda.empty_cache()
+    best = max(res, key=res.get)
+    return {"bytes_read": nbytes, "GBs": res[best], "workgroups": int(best), "GBs_by_workgroups": res}
+
+
 def per_launch_times(torch, ss, b, chunks, stream, rounds: int, batch: int):
     """Device time of each history launch of a round (HIP events recorded on
     the launch's stream around the call; one launch per call here), with the
@@ -488,7 +521,8 @@ def width_sweep(torch, H, ss, W, stream, layout: int, rounds: int = 20):
         b = H.RoundBuffers(w, kv_layout=layout, counters_zeroed=1)
         chunks = H.hbm_history(w, kv_layout=layout)
         torch.cuda.synchronize()
-        round_times(torch, H, b, chunks, stream, 10, w.num_chunks)
+        # the GPU runs its first ~40 rounds of streaming after a pause slower (see transient_blocks)
+        round_times(torch, H, b, chunks, stream, 60, w.num_chunks)
         t = round_times(torch, H, b, chunks, stream, rounds, w.num_chunks)
         del chunks
         torch.cuda.empty_cache()
@@ -557,8 +591,9 @@ def main() -> int:
                     help="only the streamed round, timed with HIP events")
     ap.add_argument("--streamed-trace", action="store_true",
                     help="only --steps streamed rounds, nothing timed in-process (for rocprofv3 memory-copy traces)")
-    ap.add_argument("--cpu-sample-requests", type=int, default=16,
-                    help="requests of the workload the fp64 oracle is timed on (16 = all of config 3, ~10 s)")
+    ap.add_argument("--cpu-sample-requests", type=int, default=0,
+                    help="requests of the workload the fp64 oracle is timed on; 0 = every request of configs "
+                         "1-4 (config 3: ~7 s, config 4: ~17 s on 16 cores), the first 16 of config 5's 32")
     ap.add_argument("--per-launch-only", action="store_true",
                     help="only time the rounds' launches (for profiler runs)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -612,6 +647,12 @@ def main() -> int:
         w = W.custom(w.hist_len, [args.num_cand] * w.B if args.num_cand > 0 else w.num_cand,
                      num_q_heads=args.num_q_heads or w.num_q_heads, num_kv_heads=w.num_kv_heads,
                      head_dim=w.head_dim, chunk_tokens=w.chunk_tokens, cfg_id=args.config)
+    probe = read = None
+    if not (args.streamed_trace or args.streamed_only or args.per_launch_only):
+        # HBM ceilings first: freeing the probes' buffers stalls the next launches for tens of ms
+        log("bench: device-to-device copy probe and read probe")
+        probe = copy_probe(torch, torch.cuda.Stream())
+        read = read_probe(torch, ss, torch.cuda.Stream())
     log(f"bench: config {args.config} ({w.name}): generating inputs on the GPU")
     if args.streamed_trace:
         b = H.RoundBuffers(w, kv_layout=layout, balance_permille=args.balance_permille)
@@ -650,8 +691,6 @@ def main() -> int:
 
     log("bench: rounds right after the input generation, blocks of 10")
     transient = transient_blocks(torch, H, b, chunks, stream, 6, 10, batch)
-    log("bench: device-to-device copy probe")
-    probe = copy_probe(torch, stream)
     log("bench: per-launch timing of the round's kernel")
     times = per_launch_times(torch, ss, b, chunks, stream, 5, batch)
     big = max(nb for _, nb in times)
@@ -732,16 +771,20 @@ def main() -> int:
             "launches_timed": len(full),
             "measured_copy_GBs": copy_gbs,
             "frac_of_measured_copy": round(achieved / copy_gbs, 4),
+            "measured_read_GBs": read["GBs"],
+            "frac_of_measured_read": round(achieved / read["GBs"], 4),
             "copy_probe": probe,
+            "read_probe": read,
         },
         "transient": {"rounds_per_block": 10, "block_mean_round_us": transient,
-                      "what": "the first 60 rounds after input generation, before every other measurement"},
+                      "what": "the first 60 rounds after input generation, before every other round measurement"},
     }
     if per_chunk is not None:
         out["per_chunk_calls"] = per_chunk
     if not args.no_cpu_baseline:
         log("bench: cpu baseline (fp64 oracle on host cores) and parity of the timed round")
-        parity, cb = cpu_baseline(w, chunks, list(range(min(w.B, args.cpu_sample_requests))), out_gpu, lse_gpu)
+        n_cpu = args.cpu_sample_requests or (16 if args.config == 5 else w.B)
+        parity, cb = cpu_baseline(w, chunks, list(range(min(w.B, n_cpu))), out_gpu, lse_gpu)
         out["cpu_baseline"] = cb
         out["parity"] = parity
     if not args.no_streamed:

@@ -99,8 +99,10 @@ typedef struct {
                                else a multiple of 32                           */
   int32_t mfma_min_rows;    /* rows per KV head (n_b * G) from which the bf16
                                MFMA path is used; fewer (at most 4) use the
-                               fp32 VALU path.  0 = default (1: always MFMA,
-                               the faster body at every row count); 2..5 =
+                               fp32 VALU path.  0 = default (3: VALU for 1-2
+                               rows, where MFMA blocks would be mostly
+                               padding and both bodies run at the HBM rate;
+                               MFMA from 3 rows); 1 = always MFMA; 2..5 =
                                VALU below that many rows; range 0..5           */
   int32_t kv_layout;        /* layout of history chunks: SS_KV_TOKEN_MAJOR
                                [sum_b len_b][Hkv][d], SS_KV_HEAD_MAJOR
@@ -317,8 +319,11 @@ ss_status ss_download_range(void *dst_pinned_host, const void *src_device, size_
  * draft time linear in q, U from the geometric acceptance model
  * (1 - a^q) / (1 - a) fitted to the measured widths).  The width changes
  * only if the estimate improves on the current one by more than
- * switch_threshold (a fraction).  Observations are exponentially weighted
- * with factor `decay` (1 = keep only the latest). */
+ * switch_threshold (a fraction).  A width's observations are averaged
+ * plainly over its first 1 / decay rounds, then exponentially weighted with
+ * factor `decay` (1 = keep only the latest); its committed-token record is
+ * blended with the acceptance model in proportion to its rounds (the model
+ * weighs as much as 16 rounds). */
 typedef struct ss_width_ctl ss_width_ctl;
 
 /* widths: host [num_widths], ascending, each in 1..8; copied. */
@@ -356,6 +361,18 @@ double ss_width_estimate(const ss_width_ctl *c, int32_t width);
  * with a balancing tail always clears it.  Every other call of the round is
  * the ordinary one; the host handle is freed with ss_round_destroy. */
 ss_status ss_round_init_scratch(ss_round **out, const ss_round_desc *desc, const void *q, hipStream_t stream);
+
+/* Measurement helper, not a step of the method: the read-bandwidth ceiling
+ * that the history launches are judged against.  Reads `bytes` of device
+ * memory at buf (16-byte aligned, a non-zero multiple of 16) with the
+ * history kernel's load form (16 bytes per lane, non-temporal), split over
+ * `workgroups` (1..65536) workgroups of 256 threads in equal contiguous
+ * slices of ceil(bytes / 16 / workgroups) * 16 bytes (at most 1 GiB each;
+ * trailing workgroups may get empty slices).  Workgroup w stores the XOR of
+ * its slice's 32-bit words to sink[w] (device, 4-byte aligned, `workgroups`
+ * words), so the reads cannot be elided and the result is checkable.
+ * Enqueues one launch on `stream`; both buffers stay the caller's. */
+ss_status ss_probe_read(const void *buf, size_t bytes, uint32_t *sink, int32_t workgroups, hipStream_t stream);
 
 /* Event helpers so callers need no HIP binding of their own.  Events are
  * created with timing disabled. */

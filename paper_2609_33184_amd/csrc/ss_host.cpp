@@ -87,11 +87,15 @@ constexpr long kTailMin = 256;
 constexpr long kTailMax = 4096;
 constexpr long kTailMinShare = 16384;          // with the default tail
 constexpr long kTailMinShareExplicit = 4096;   // with a tail the caller asked for
-// Body for few rows per KV head: the MFMA body with padded rows by default.
-// With non-temporal K/V loads the fp32 VALU body became compute-bound (VALU
-// 72% busy): 16 x 32768 tokens with 4 rows per KV head took 396-399 us on
-// VALU and 330-345 us on MFMA; 64 ragged requests 710 and 695 us.
-constexpr int kDefaultMfmaMinRows = 1;
+// Density dispatch: units of 1 or 2 rows per KV head run the fp32 VALU body
+// (built for that many rows), units of 3 or more the bf16 MFMA body, whose
+// 16-row blocks would be 7/8 padding or more below that.  Measured on
+// MI355X, one launch over 16 x 32768 tokens (same box, same run): 1 row per
+// KV head 305.4 us on VALU against 307.1 us on MFMA, 2 rows 305.3-305.9
+// against 301.8-305.9 us; at 4 rows the VALU body is bound by its own
+// arithmetic (358.2 against 301.4 us), so it takes no unit of 3-4 rows by
+// default.
+constexpr int kDefaultMfmaMinRows = 3;
 
 ss_status validate_desc(const ss_round_desc *d) {
   if (d == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "desc is null");
@@ -940,6 +944,30 @@ void ss_pipeline_destroy(ss_pipeline *p) {
     (void)hipEventDestroy(p->freed[i]);
   }
   delete p;
+}
+
+ss_status ss_probe_read(const void *buf, size_t bytes, uint32_t *sink, int32_t workgroups, hipStream_t stream) {
+  if (buf == nullptr || sink == nullptr) return fail(SS_ERR_INVALID_ARGUMENT, "buffer and sink must be non-null");
+  if (bytes == 0 || bytes % 16 != 0 || reinterpret_cast<uintptr_t>(buf) % 16 != 0)
+    return fail(SS_ERR_INVALID_ARGUMENT, "the buffer must be 16-byte aligned and a non-zero multiple of 16 bytes");
+  if (reinterpret_cast<uintptr_t>(sink) % 4 != 0) return fail(SS_ERR_INVALID_ARGUMENT, "sink is not 4-byte aligned");
+  if (workgroups < 1 || workgroups > 65536) return fail(SS_ERR_INVALID_ARGUMENT, "workgroups must be in 1..65536");
+  const uint64_t share = (bytes / 16 + (uint64_t)workgroups - 1) / (uint64_t)workgroups * 16;
+  if (share > ss::kProbeMaxShare)
+    return fail(SS_ERR_INVALID_ARGUMENT, "%llu bytes per workgroup; at most %llu", (unsigned long long)share,
+                (unsigned long long)ss::kProbeMaxShare);
+  for (const void *ptr : {static_cast<const void *>(buf), static_cast<const void *>(sink)}) {
+    hipPointerAttribute_t attr;
+    std::memset(&attr, 0, sizeof attr);
+    const hipError_t e = hipPointerGetAttributes(&attr, ptr);
+    if (e != hipSuccess || attr.type != hipMemoryTypeDevice) {
+      (void)hipGetLastError();
+      return fail(SS_ERR_INVALID_ARGUMENT, "%p is not device memory", ptr);
+    }
+  }
+  const hipError_t e = ss::launch_read_probe(buf, bytes, share, sink, workgroups, stream);
+  if (e != hipSuccess) return hip_fail(e, "read probe launch");
+  return SS_OK;
 }
 
 ss_status ss_event_create(hipEvent_t *e) {

@@ -133,6 +133,13 @@ hipError_t launch_finalize(const FinalParams &p, hipStream_t s);
 // captured in a graph).
 hipError_t launch_clear_counters(uint32_t *counters, int n, hipStream_t s);
 
+// Read-bandwidth probe over `bytes` (a multiple of 16) of device memory:
+// workgroup w < workgroups XOR-folds bytes [w * share, (w + 1) * share)
+// (share a multiple of 16, at most kProbeMaxShare) into sink[w].
+constexpr uint64_t kProbeMaxShare = uint64_t(1) << 30;
+hipError_t launch_read_probe(const void *buf, uint64_t bytes, uint64_t share, uint32_t *sink, int workgroups,
+                             hipStream_t s);
+
 // The library's own device scratch: a file-scope device array of
 // kScratchBytes that serves as the workspace of rounds started with
 // ss_round_init_scratch.  scratch_address returns its address on the

@@ -917,8 +917,7 @@ static_assert(kRowsLdsBytes <= kChunkLdsBytes && 2 * kChunkLdsBytes <= 160 * 102
 // call's tokens, which may span several requests); each unit's kind selects
 // the body: MFMA with two or one 16-row blocks, the row-split body for
 // three or four (only on the wide instantiation, which a launch with such a
-// unit runs on), or the VALU path for <= 4 rows (when the round asks for
-// it).  The heads are the fast grid dimension:
+// unit runs on), or the VALU path for <= 4 rows (built for 1, 2 and 4 rows).  The heads are the fast grid dimension:
 // with 8 KV heads the round-robin placement gives every XCD one head of
 // every workgroup's share.
 //
@@ -987,8 +986,18 @@ __global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
       mfma_unit<2>(p, smem, i0, nit, tx, g);
     else if (kind == kUnitMfma1)
       mfma_unit<1>(p, smem, i0, nit, tx, g);
-    else
-      valu_unit<kMaxValuRows>(p, reinterpret_cast<float *>(smem), i0, nit, tx, g);
+    else {
+      // the VALU body's work grows with the rows it is built for: build it
+      // for 1, 2 and 4 rows and take the smallest that holds the unit
+      const int rows = p.items[i0].n_cand * p.G;
+      float *lds = reinterpret_cast<float *>(smem);
+      if (rows <= 1)
+        valu_unit<1>(p, lds, i0, nit, tx, g);
+      else if (rows <= 2)
+        valu_unit<2>(p, lds, i0, nit, tx, g);
+      else
+        valu_unit<kMaxValuRows>(p, lds, i0, nit, tx, g);
+    }
   }
 }
 
@@ -1105,6 +1114,42 @@ __global__ void __launch_bounds__(256) finalize_kernel(const P p) {
   if (p.lse != nullptr && lane == 0) p.lse[row] = m * 0.69314718055994531f + logf(l);
 }
 
+// Read-bandwidth probe: workgroup w XOR-folds the 32-bit words of bytes
+// [w * share, min((w + 1) * share, bytes)) of buf and stores the fold to
+// sink[w].  The loads are the history kernel's: 16 bytes per lane, non-
+// temporal, through a range-checked buffer resource (reads past the slice
+// return zero, which the fold ignores), eight per lane in flight.
+__global__ void __launch_bounds__(256) read_probe_kernel(const uint8_t *buf, uint64_t bytes, uint64_t share,
+                                                         uint32_t *sink) {
+  const uint64_t first = (uint64_t)blockIdx.x * share;
+  const uint32_t n = first >= bytes ? 0u : (uint32_t)(bytes - first < share ? bytes - first : share);
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(buf) + (first < bytes ? first : 0), (short)0, (int)n,
+                                        kBufferFlags);
+  constexpr uint32_t kStep = 256 * 16;   // bytes one load instruction of the workgroup reads
+  constexpr int kDepth = 8;
+  const uint32_t t = threadIdx.x * 16u;
+  u32x4_t acc = {0u, 0u, 0u, 0u};
+  uint32_t o = 0;
+  for (; o + kDepth * kStep <= n; o += kDepth * kStep) {
+    u32x4_t v[kDepth];
+#pragma unroll
+    for (int i = 0; i < kDepth; ++i)
+      v[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, o + i * kStep + t, 0, kStreamLoad));
+#pragma unroll
+    for (int i = 0; i < kDepth; ++i) acc ^= v[i];
+  }
+  for (; o < n; o += kStep)
+    acc ^= __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, o + t, 0, kStreamLoad));
+  uint32_t x = acc.x ^ acc.y ^ acc.z ^ acc.w;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x ^= (uint32_t)__shfl_xor((int)x, m, 64);
+  __shared__ uint32_t part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
+}
+
 // The library's device scratch (see scratch_address).  Each GPU the library
 // runs on holds its own copy until the process ends.
 __device__ __align__(256) unsigned char scratch[kScratchBytes];
@@ -1167,6 +1212,13 @@ hipError_t launch_finalize(const FinalParams &p, hipStream_t s) {
   } else {
     hipLaunchKernelGGL(finalize_kernel<FinalParams>, grid, dim3(256), 0, s, p);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_read_probe(const void *buf, uint64_t bytes, uint64_t share, uint32_t *sink, int workgroups,
+                             hipStream_t s) {
+  hipLaunchKernelGGL(read_probe_kernel, dim3(workgroups), dim3(256), 0, s, static_cast<const uint8_t *>(buf), bytes,
+                     share, sink);
   return hipGetLastError();
 }
 

@@ -16,9 +16,11 @@
 // commits at least one token).  Its per-token acceptance a is fitted to all
 // measured widths, each weighted by its number of rounds, so the rounds run
 // at the current width keep every other width's estimate current; a width's
-// own record is blended with the model's value in proportion to its rounds.
+// own record (the mean of its first rounds, exponentially weighted after
+// that) is blended with the model's value in proportion to its rounds.
 // The width changes only when the estimate improves on the current width's
 // by more than the switching threshold.
+#include <algorithm>
 #include <cmath>
 #include <new>
 #include <vector>
@@ -44,7 +46,11 @@ struct ss_width_ctl {
 namespace {
 
 constexpr int32_t kMaxWeight = 32;   // rounds beyond this add no weight to a width's record
-constexpr double kPriorRounds = 4;   // weight of the acceptance model against a width's own record
+// Weight, in rounds, of the acceptance model against a width's own record of
+// committed tokens.  A round's count varies a lot (at a = 0.9 and q = 8 its
+// standard deviation is 45% of its mean), so a width sampled a few times
+// leans on the model fitted over every round until its own rounds add up.
+constexpr double kPriorRounds = 16;
 
 // Expected committed tokens of a round with q candidate rows (q - 1 draft
 // tokens) under per-token acceptance a: 1 + a + ... + a^(q-1).
@@ -53,9 +59,25 @@ double committed_model(double a, int q) {
   return (1.0 - std::pow(a, q)) / (1.0 - a);
 }
 
+// Variance of a round's committed tokens under the model: n = 1 + the
+// accepted drafts before the first rejection, at most q, so P(n >= k) =
+// a^(k-1) for k = 1..q and E[n^2] = sum_k (2k - 1) a^(k-1).
+double committed_var(double a, int q) {
+  double m = 0, m2 = 0, p = 1;
+  for (int k = 1; k <= q; ++k) {
+    m += p;
+    m2 += (2.0 * k - 1.0) * p;
+    p *= a;
+  }
+  return m2 - m * m;
+}
+
 // Per-token acceptance whose model matches the measured committed counts
-// best (least squares over the measured widths; a grid over [0, 1] refined
-// once around its best point).
+// best: weighted least squares over the measured widths, each width's
+// squared deviation weighted by its rounds over the model's variance of one
+// round's count (a narrow width's steady record pins a as well as a few
+// rounds of a wide one); a grid over [0, 1] refined once around its best
+// point.
 double fit_acceptance(const ss_width_ctl *c) {
   double best_a = 0.5, best_e = INFINITY;
   for (int pass = 0; pass < 2; ++pass) {
@@ -66,8 +88,9 @@ double fit_acceptance(const ss_width_ctl *c) {
       double e = 0;
       for (size_t k = 0; k < c->widths.size(); ++k)
         if (c->st[k].n > 0) {
-          const double d = committed_model(a, c->widths[k]) - c->st[k].committed;
-          e += std::min(c->st[k].n, kMaxWeight) * d * d;
+          const int q = c->widths[k];
+          const double d = committed_model(a, q) - c->st[k].committed;
+          e += std::min(c->st[k].n, kMaxWeight) * d * d / (committed_var(a, q) + 0.05);
         }
       if (e < best_e) {
         best_e = e;
@@ -168,7 +191,10 @@ ss_status ss_width_observe(ss_width_ctl *c, int32_t width, double transfer_s, do
   if (!(transfer_s >= 0) || !(compute_s >= 0) || !(draft_s >= 0) || !(correct_s >= 0) || !(committed_tokens >= 0))
     return fail(SS_ERR_INVALID_ARGUMENT, "observations must be finite and >= 0");
   ss_width_ctl::Stat &s = c->st[k];
-  const double w = s.n == 0 ? 1.0 : c->decay;
+  // the plain mean of the first rounds, then the exponential weighting (a
+  // weight of `decay` from the start would leave the first round's value
+  // with most of the weight for about 1 / decay rounds)
+  const double w = std::max(c->decay, 1.0 / (s.n + 1));
   s.transfer += w * (transfer_s - s.transfer);
   s.compute += w * (compute_s - s.compute);
   s.draft += w * (draft_s - s.draft);

@@ -32,7 +32,7 @@ SS_KV_HEAD_MAJOR_KV = 2  # history chunk [Hkv][sum len][2][d]: K and V rows of a
 EXPORTED = (
     "ss_round_workspace_bytes", "ss_round_init", "ss_upload_chunk", "ss_attend_history_chunk",
     "ss_attend_history_chunks",
-    "ss_attend_local_candidates", "ss_round_finalize", "ss_round_init_scratch",
+    "ss_attend_local_candidates", "ss_round_finalize", "ss_round_init_scratch", "ss_probe_read",
     "ss_round_destroy", "ss_pipeline_create",
     "ss_pipeline_attend_chunk", "ss_pipeline_attend_chunks", "ss_pipeline_destroy", "ss_event_create", "ss_event_destroy",
     "ss_status_string", "ss_last_error",
@@ -104,6 +104,7 @@ def load() -> ctypes.CDLL:
         "ss_attend_local_candidates": (I32, [P, P, P, P]),
         "ss_round_finalize": (I32, [P, P, P, P]),
         "ss_round_init_scratch": (I32, [ctypes.POINTER(P), ctypes.POINTER(ss_round_desc), P, P]),
+        "ss_probe_read": (I32, [P, SZ, P, I32, P]),
         "ss_round_destroy": (None, [P]),
         "ss_pipeline_create": (I32, [ctypes.POINTER(P), P, P, SZ, P]),
         "ss_pipeline_attend_chunk": (I32, [P, P, P, PI32, P]),
@@ -202,6 +203,10 @@ def ss_round_init_scratch(desc: ss_round_desc, q: int, stream: int = 0) -> int:
     h = ctypes.c_void_p()
     _check(load().ss_round_init_scratch(ctypes.byref(h), ctypes.byref(desc), q, stream), "ss_round_init_scratch")
     return h.value
+
+
+def ss_probe_read(buf: int, nbytes: int, sink: int, workgroups: int, stream: int = 0) -> None:
+    _check(load().ss_probe_read(buf, nbytes, sink, workgroups, stream), "ss_probe_read")
 
 
 def ss_round_destroy(r: Optional[int]) -> None:

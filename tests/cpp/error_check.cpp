@@ -41,6 +41,7 @@ namespace ss {
 hipError_t launch_chunk(const ChunkParams &, hipStream_t) { return launch_result(); }
 hipError_t launch_finalize(const FinalParams &, hipStream_t) { return launch_result(); }
 hipError_t launch_clear_counters(uint32_t *, int, hipStream_t) { return launch_result(); }
+hipError_t launch_read_probe(const void *, uint64_t, uint64_t, uint32_t *, int, hipStream_t) { return launch_result(); }
 hipError_t scratch_address(void **) { return hipErrorNotSupported; }
 }  // namespace ss
 

@@ -53,6 +53,7 @@ hipError_t launch_clear_counters(uint32_t *c, int n, hipStream_t) {
   ++g_clears; g_clear_ptr = c; g_clear_n = n; return hipSuccess;
 }
 // The scratch stands at the same address as the caller workspaces below.
+hipError_t launch_read_probe(const void *, uint64_t, uint64_t, uint32_t *, int, hipStream_t) { return hipSuccess; }
 hipError_t scratch_address(void **p) { *p = (void *)0x7f1000000000ull; return hipSuccess; }
 }
 

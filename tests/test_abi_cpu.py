@@ -187,3 +187,15 @@ def test_scratch_round_rejects_rounds_beyond_the_scratch(lib):
     with pytest.raises(ss.SpecStreamError) as e:
         ss.ss_round_init_scratch(ss.make_desc([0], 8, 2), FAKE_Q)
     assert e.value.status == ss.SS_ERR_INVALID_ARGUMENT
+
+
+def test_read_probe_argument_checks(lib):
+    """ss_probe_read refuses bad sizes, alignment and grids before it looks
+    at the pointers."""
+    cases = [(0, 16, FAKE_WS, 1), (FAKE_WS, 0, FAKE_WS, 1), (FAKE_WS, 24, FAKE_WS, 1), (FAKE_WS + 8, 32, FAKE_WS, 1),
+             (FAKE_WS, 32, FAKE_WS, 0), (FAKE_WS, 32, FAKE_WS, 65537), (FAKE_WS, 32, FAKE_WS + 2, 1),
+             (FAKE_WS, (2 << 30) + 16, FAKE_WS, 2)]
+    for buf, n, sink, g in cases:
+        with pytest.raises(ss.SpecStreamError) as e:
+            ss.ss_probe_read(buf, n, sink, g)
+        assert e.value.status == ss.SS_ERR_INVALID_ARGUMENT, (buf, n, sink, g)

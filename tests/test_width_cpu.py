@@ -103,41 +103,50 @@ def test_estimates_for_unmeasured_widths_follow_the_model(lib):
 
 
 def test_noisy_rounds_settle_near_the_optimum(lib):
-    rng = random.Random(5)
+    """Sampled committed counts, 10 seeds per environment: the widths of the
+    last 100 of 600 rounds cost on average at most 3% more per committed
+    token than the optimum, and at most 8% more in 9 runs of 10."""
+    ratios = []
     for env in ENVS:
-        c = ss.ss_width_create(WIDTHS, switch_threshold=0.03, min_samples=3, decay=0.05)
-        try:
-            picks = []
-            for _ in range(600):
-                q = ss.ss_width_select(c)
-                picks.append(q)
-                ss.ss_width_observe(c, q, *env.parts(q), env.sample_committed(q, rng))
-            final = picks[-100:]
-            worst = max(env.cost(q) for q in set(final))
-            assert worst <= env.cost(env.best()) * 1.08, (final[-5:], env.best())
-        finally:
-            ss.ss_width_destroy(c)
+        for seed in range(10):
+            rng = random.Random(seed)
+            c = ss.ss_width_create(WIDTHS, switch_threshold=0.03, min_samples=3, decay=0.02)
+            try:
+                picks = []
+                for _ in range(600):
+                    q = ss.ss_width_select(c)
+                    picks.append(q)
+                    ss.ss_width_observe(c, q, *env.parts(q), env.sample_committed(q, rng))
+            finally:
+                ss.ss_width_destroy(c)
+            ratios.append(sum(env.cost(q) for q in picks[-100:]) / 100 / env.cost(env.best()))
+    assert sum(ratios) / len(ratios) <= 1.03
+    assert sum(r <= 1.08 for r in ratios) >= 0.9 * len(ratios)
 
 
 def test_switching_threshold_keeps_the_current_width(lib):
-    """Width 4 is current; width 5's latest record becomes 1.5% cheaper per
-    committed token: with a 5% threshold the controller stays, without a
-    threshold it moves."""
+    """Width 4 is current; width 5 is re-measured as 1.5% cheaper per
+    committed token (committed tokens as the acceptance model predicts, a
+    slightly cheaper draft): with a 5% threshold the controller stays,
+    without a threshold it moves."""
     env = Env(0.038, 0.0004, 0.00002, 0.002, 0.0005, 0.8)
     t, cp, d, k = env.parts(4)
-    u4 = env.expected_committed(4)
+    u4, u5 = env.expected_committed(4), env.expected_committed(5)
+    round5 = 0.985 * env.cost(4) * u5
+    d5 = round5 - max(t, cp) - k
+    assert d5 > 0
     for thr, moves in ((0.05, False), (0.0, True)):
         c = ss.ss_width_create([4, 5], switch_threshold=thr, min_samples=1, decay=1.0)
         try:
             assert ss.ss_width_select(c) == 4
             ss.ss_width_observe(c, 4, t, cp, d, k, u4)
             assert ss.ss_width_select(c) == 5
-            ss.ss_width_observe(c, 5, t, cp, d, k, u4 * 0.5)      # width 5 looks poor at first
+            ss.ss_width_observe(c, 5, t, cp, 2 * d5, k, u5)      # width 5 looks poor at first
             assert ss.ss_width_select(c) == 4
-            for _ in range(40):                                    # then is re-measured as slightly better
-                ss.ss_width_observe(c, 5, t, cp, d, k, u4 * 1.015)
+            for _ in range(40):                                # then is re-measured as slightly better
+                ss.ss_width_observe(c, 5, t, cp, d5, k, u5)
                 ss.ss_width_observe(c, 4, t, cp, d, k, u4)
-            assert ss.ss_width_estimate(c, 5) < ss.ss_width_estimate(c, 4) < ss.ss_width_estimate(c, 5) * 1.05
+            assert ss.ss_width_estimate(c, 5) == pytest.approx(0.985 * ss.ss_width_estimate(c, 4), rel=1e-3)
             assert (ss.ss_width_select(c) == 5) == moves
         finally:
             ss.ss_width_destroy(c)
