@@ -385,8 +385,11 @@ bool build_plan(const ss_round *r, int nchunks, const int32_t *len, long W, long
   return true;
 }
 
+size_t unit_records(const Plan &plan, size_t w0, size_t w1);
+
 bool fits_one_launch(const Plan &plan) {
-  return plan.wg_first.size() - 1 <= (size_t)ss::kMaxWgs && plan.units() <= (size_t)ss::kMaxUnits &&
+  const size_t W = plan.wg_first.size() - 1;
+  return W <= (size_t)ss::kMaxWgs && unit_records(plan, 0, W) + plan.num_tail <= (size_t)ss::kMaxUnits &&
          plan.items.size() <= (size_t)ss::kMaxItems;
 }
 
@@ -457,6 +460,7 @@ ss::ChunkParams *base_params(const ss_round *r, int nchunks, const void *const *
   p.G = r->G;
   p.scale_log2 = r->scale * 1.4426950408889634f;
   p.tok_stride = tok_stride(r);
+  p.heads_fast = r->kv_layout == SS_KV_TOKEN_MAJOR ? 1 : 0;
   for (int c = 0; c < nchunks; ++c) {
     p.k[c] = static_cast<const uint16_t *>(k[c]);
     p.v[c] = static_cast<const uint16_t *>(v[c]);
@@ -471,35 +475,68 @@ ss::ChunkParams *base_params(const ss_round *r, int nchunks, const void *const *
 }
 
 // Launch the workgroups of `plan` in batches of at most kMaxWgs workgroups,
-// kMaxUnits units and kMaxItems items with `launch(params)`.  A plan with a
-// balancing tail is launched whole, tail units after the workgroups' own.
+// kMaxUnits unit records and kMaxItems items with `launch(params)`.  A
+// batch's records are the first unit of each of its workgroups (an empty
+// record for a workgroup without units), then the further units in
+// workgroup order, then the balancing tail.  A plan with a balancing tail
+// is launched whole, tail units after the workgroups' own.
+size_t unit_records(const Plan &plan, size_t w0, size_t w1) {
+  size_t n = plan.wg_first[w1] - plan.wg_first[w0];
+  for (size_t w = w0; w < w1; ++w) n += plan.wg_first[w + 1] == plan.wg_first[w];
+  return n;
+}
+
 template <typename F>
 hipError_t launch_units(ss::ChunkParams *p, const Plan &plan, F launch) {
   const size_t W = plan.wg_first.size() - 1;
+  const size_t tail = plan.num_tail;
   size_t w0 = 0;
   while (w0 < W) {
     const uint32_t u0 = plan.wg_first[w0];
     const uint32_t i0 = plan.unit_first[u0];
-    size_t w1 = w0;
-    while (w1 < W && w1 - w0 < (size_t)ss::kMaxWgs && plan.wg_first[w1 + 1] - u0 <= (uint32_t)ss::kMaxUnits &&
-           plan.unit_first[plan.wg_first[w1 + 1]] - i0 <= (uint32_t)ss::kMaxItems)
+    size_t w1 = w0, nrec = 0;   // records of workgroups [w0, w1)
+    for (;;) {
+      if (w1 == W || w1 - w0 == (size_t)ss::kMaxWgs) break;
+      const size_t add = std::max<size_t>(1, plan.wg_first[w1 + 1] - plan.wg_first[w1]);
+      if (nrec + add + tail > (size_t)ss::kMaxUnits ||
+          plan.unit_first[plan.wg_first[w1 + 1]] - i0 > (uint32_t)ss::kMaxItems)
+        break;
+      nrec += add;
       ++w1;
+    }
     if (w1 == w0) return hipErrorInvalidValue;   // one share over the table sizes (plan_chunks prevents it)
     const uint32_t u1 = plan.wg_first[w1];
-    const bool tail = plan.num_tail > 0;
-    if (tail && !(w0 == 0 && w1 == W)) return hipErrorInvalidValue;   // plan_chunks keeps such plans whole
-    const uint32_t uend = tail ? (uint32_t)plan.units() : u1;
+    if (tail > 0 && !(w0 == 0 && w1 == W)) return hipErrorInvalidValue;   // plan_chunks keeps such plans whole
+    const uint32_t uend = tail > 0 ? (uint32_t)plan.units() : u1;
     const uint32_t n = plan.unit_first[uend] - i0;
     std::memcpy(p->items, plan.items.data() + i0, n * sizeof(ss::Item));
-    for (uint32_t u = u0; u < uend; ++u)
-      p->units[u - u0] = (plan.unit_first[u] - i0) | ((plan.unit_first[u + 1] - plan.unit_first[u]) << 16) |
-                         ((uint32_t)plan.kind[u] << 24);
-    for (size_t w = w0; w <= w1; ++w) p->wg_first[w - w0] = (uint16_t)(plan.wg_first[w] - u0);
+    auto rec = [&](uint32_t u) {
+      ss::UnitRec ur;
+      const uint32_t f = plan.unit_first[u], nit = plan.unit_first[u + 1] - f;
+      uint32_t ntiles = 0;
+      for (uint32_t i = f; i < f + nit; ++i) ntiles += (uint32_t)((plan.items[i].tok_count + ss::kTile - 1) / ss::kTile);
+      ur.word = ss::unit_word(f - i0, nit, plan.kind[u], plan.items[f].chunk);
+      ur.ntiles = ntiles;
+      ur.q_row0 = plan.items[f].q_row0;
+      ur.n_cand = plan.items[f].n_cand;
+      return ur;
+    };
+    const size_t nw = w1 - w0;
+    size_t next = nw;   // further units start after the first-unit records
+    for (size_t w = w0; w < w1; ++w) {
+      const uint32_t a = plan.wg_first[w], b = plan.wg_first[w + 1];
+      p->units[w - w0] = a < b ? rec(a) : ss::UnitRec{0u, 0u, 0, 0};
+      p->more[w - w0] = (uint32_t)next;
+      for (uint32_t u = a + 1; u < b; ++u) p->units[next++] = rec(u);
+    }
+    p->more[nw] = (uint32_t)next;
+    const size_t tail_first = next;
+    for (uint32_t u = u1; u < uend; ++u) p->units[next++] = rec(u);
     p->num_items = (int32_t)n;
-    p->num_units = (int32_t)(uend - u0);
-    p->num_wgs = (int32_t)(w1 - w0);
-    p->tail_first = tail ? (int32_t)(plan.tail_first - u0) : 0;
-    p->num_tail = tail ? (int32_t)plan.num_tail : 0;
+    p->num_units = (int32_t)next;
+    p->num_wgs = (int32_t)nw;
+    p->tail_first = tail > 0 ? (int32_t)tail_first : 0;
+    p->num_tail = tail > 0 ? (int32_t)tail : 0;
     const hipError_t e = launch(*p);
     if (e != hipSuccess) return e;
     w0 = w1;

@@ -79,8 +79,14 @@ struct ChunkHeader {
   const uint16_t *k[kMaxChunks];
   const uint16_t *v[kMaxChunks];
   uint64_t head_stride[kMaxChunks];   // elements between KV heads at the same token
-  int32_t num_units;
-  int32_t num_wgs;      // workgroups per KV head (grid.y)
+  int32_t num_units;    // unit records (num_wgs first-unit records included)
+  int32_t num_wgs;      // workgroups per KV head
+  // Grid order: 1 = (KV head, workgroup) with the heads as the fast
+  // dimension, 0 = (workgroup, KV head).  Workgroups are placed on the XCDs
+  // round-robin in grid order, so with the heads fast XCD g streams only KV
+  // head g; that suits token-major chunks, where a token's heads are
+  // adjacent, and not head-major ones, where each head is its own plane.
+  int32_t heads_fast;
   // Balancing tail: units [tail_first, tail_first + num_tail) are claimed at
   // run time, for every KV head, by whichever workgroup has finished its own
   // units: claim c = atomicAdd(claim, 1) < num_tail * Hkv attends unit
@@ -91,16 +97,38 @@ struct ChunkHeader {
   int32_t num_tail;
 };
 
+// Unit record: what a workgroup needs to start a unit, so that its first
+// loads depend on one record and the item and chunk-table entries it names
+// (kernel arguments are read with dependent loads of about a microsecond
+// each at the start of a launch).  word packs the unit's first item i0
+// (within the launch), its item count nit (1..kMaxChain; 0 = no unit), the
+// body kind and the chunk of item i0; ntiles is the chain's tile count.
+struct UnitRec {
+  uint32_t word;
+  uint32_t ntiles;
+  int32_t q_row0;   // off_b of the unit's request
+  int32_t n_cand;   // n_b of the unit's request
+};
+static_assert(sizeof(UnitRec) == 16, "UnitRec layout");
+constexpr uint32_t unit_word(uint32_t i0, uint32_t nit, uint32_t kind, uint32_t chunk) {
+  return i0 | (nit << 16) | (kind << 21) | (chunk << 24);
+}
+constexpr int unit_i0(uint32_t w) { return (int)(w & 0xffffu); }
+constexpr int unit_nit(uint32_t w) { return (int)((w >> 16) & 0x1fu); }
+constexpr int unit_kind(uint32_t w) { return (int)((w >> 21) & 0x7u); }
+constexpr int unit_chunk(uint32_t w) { return (int)((w >> 24) & 0x1fu); }
+static_assert(kMaxItems <= 0x10000 && kMaxChain <= 0x1f && kUnitMfma4 <= 7 && kMaxChunks <= 0x20, "unit word fields");
+
 template <int MaxUnits, int MaxItems, int MaxWgs>
 struct ChunkParamsT : ChunkHeader {
   static constexpr int kUnits = MaxUnits;
   static constexpr int kItems = MaxItems;
   static constexpr int kWgs = MaxWgs;
-  // unit u = items [units[u] & 0xffff, + ((units[u] >> 16) & 0xff)), 1..kMaxChain
-  // items, attended by the body units[u] >> 24 (kUnitValu / kUnitMfma1..4)
-  uint32_t units[MaxUnits];
-  // workgroup w (of every KV head) attends units [wg_first[w], wg_first[w + 1]) in order
-  uint16_t wg_first[MaxWgs + 1];
+  // Units of workgroup w (of every KV head): units[w] (its first unit; a
+  // record with nit = 0 if it has none), then units [more[w], more[w + 1]).
+  // Units [num_wgs, tail_first) are these further units in workgroup order.
+  UnitRec units[MaxUnits];
+  uint32_t more[MaxWgs + 1];
   Item items[MaxItems];
 };
 using ChunkParams = ChunkParamsT<kMaxUnits, kMaxItems, kMaxWgs>;   // what the host fills
@@ -125,7 +153,7 @@ struct FinalParamsT : FinalHeader {
 using FinalParams = FinalParamsT<kMaxItems>;
 
 // Launch wrappers; return hipGetLastError() of the launch.
-// History units of every kind, grid (Hkv, num_wgs).
+// History units of every kind, grid (Hkv, num_wgs) or (num_wgs, Hkv) by heads_fast.
 hipError_t launch_chunk(const ChunkParams &p, hipStream_t s);
 // Speculative Frontier pass fused with the split-slot merge and O = a / l.
 hipError_t launch_finalize(const FinalParams &p, hipStream_t s);

@@ -78,11 +78,11 @@ __device__ __forceinline__ float xgroup_sum(float x) {
 }
 
 template <typename P>
-__device__ __forceinline__ int global_row(const P &p, const Item &it, int g, int r) {
+__device__ __forceinline__ int global_row(const P &p, int q_row0, int g, int r) {
   // local row r of (request, kv head g) -> packed query row (off_b + i) * Hq + h
   const int i = r / p.G;
   const int h = g * p.G + (r - i * p.G);
-  return (it.q_row0 + i) * p.Hq + h;
+  return (q_row0 + i) * p.Hq + h;
 }
 
 // ---------------------------------------------------------------------------
@@ -92,7 +92,7 @@ __device__ __forceinline__ int global_row(const P &p, const Item &it, int g, int
 // fold the result into the item's slot of the running state (Eq. 14 again).
 // ---------------------------------------------------------------------------
 template <int ROWS, typename P>
-__device__ __forceinline__ void fold_into_slot(const P &p, const Item &it, int g, int M, int tx,
+__device__ __forceinline__ void fold_into_slot(const P &p, const Item &it, int q_row0, int g, int M, int tx,
                                                const float *aw, const float *mw, const float *lw) {
   // SEGS threads per row (the largest power of two with SEGS * ROWS <= 256,
   // at most 32), SEGLEN (a multiple of 4) values each
@@ -131,7 +131,7 @@ __device__ __forceinline__ void fold_into_slot(const P &p, const Item &it, int g
       a[c + 3] += f[w] * x[3];
     }
   }
-  const size_t idx = (size_t)it.slot * p.st.R + global_row(p, it, g, r);
+  const size_t idx = (size_t)it.slot * p.st.R + global_row(p, q_row0, g, r);
   float *ap = p.st.a + idx * kHeadDim + seg * SEGLEN;
   if (it.flags & kSlotFresh) {       // first write of this slot in the round: store
 #pragma unroll
@@ -214,18 +214,48 @@ __device__ __forceinline__ int item_chunk(const Item &it) {
 }
 static_assert(offsetof(Item, chunk) == 13, "Item layout");
 
-// Buffer resource over item `it`'s rows of KV head g in chunk table `tab`
-// (p.k or p.v): loads past the item's last token return zero, so no
-// clamping is needed.  Offsets are 32-bit (the host keeps an item below
-// 2^31 bytes).
+// Buffer resource over item `it`'s rows of KV head g in the chunk that
+// starts at `base` (K or V) with head_stride `hs` elements: loads past the
+// item's last token return zero, so no clamping is needed.  Offsets are
+// 32-bit (the host keeps an item below 2^31 bytes).
 template <typename P>
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t item_rsrc(const P &p, const Item &it, int g,
-                                                            const uint16_t *const *tab) {
-  const int chunk = item_chunk(it);
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t item_rsrc_at(const P &p, const Item &it, const uint16_t *base,
+                                                               uint64_t hs, int g) {
   const uint32_t nrec = (uint32_t)(it.tok_count - 1) * (p.tok_stride * 2) + kRowBytes;
-  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * p.head_stride[chunk];
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(tab[chunk] + first), (short)0, (int)nrec,
-                                           kBufferFlags);
+  const size_t first = (size_t)it.tok_begin * p.tok_stride + (size_t)g * hs;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(base + first), (short)0, (int)nrec, kBufferFlags);
+}
+// The same through the launch's chunk table `tab` (p.k or p.v).
+template <typename P>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t item_rsrc(const P &p, const Item &it, int chunk, int g,
+                                                            const uint16_t *const *tab) {
+  return item_rsrc_at(p, it, tab[chunk], p.head_stride[chunk], g);
+}
+
+// A unit's first item and its chunk-table entries.  The item is read as
+// whole dwords, and the item and the three entries are forced into
+// registers at one point, so their loads go out together (the chunk comes
+// from the unit record, not from the item) and are waited for once.
+struct FirstItem {
+  Item it;
+  const uint16_t *k, *v;
+  uint64_t hs;
+};
+template <typename P>
+__device__ __forceinline__ FirstItem load_first_item(const P &p, const UnitRec &ur) {
+  const int i0 = unit_i0(ur.word), c = unit_chunk(ur.word);
+  uint32_t w[4];
+  __builtin_memcpy(w, &p.items[i0], sizeof w);
+  const uint16_t *k = p.k[c];
+  const uint16_t *v = p.v[c];
+  uint64_t hs = p.head_stride[c];
+  asm volatile("" : "+s"(w[0]), "+s"(w[1]), "+s"(w[2]), "+s"(w[3]), "+s"(k), "+s"(v), "+s"(hs));
+  FirstItem f;
+  __builtin_memcpy(&f.it, w, sizeof w);
+  f.k = k;
+  f.v = v;
+  f.hs = hs;
+  return f;
 }
 
 // A unit's tiles are numbered across its chain of items (item 0's tiles
@@ -265,15 +295,15 @@ __device__ __forceinline__ s16x4_t lds_read_tr16(const unsigned char *p) {
 }
 
 template <int RB, typename P>
-__device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i0, int nit, int tx, int g) {
+__device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, const UnitRec &ur, int tx, int g) {
   const int w = __builtin_amdgcn_readfirstlane(tx >> 6);   // wave-uniform
   const int lane = tx & 63;
   const int lr = lane & 15;
   const int lq = lane >> 4;
-  const Item it = p.items[i0];          // request, slot and flags of the whole chain
-  const int M = it.n_cand * p.G;
-  int ntiles = 0;
-  for (int k = 0; k < nit; ++k) ntiles += tiles_of(p.items[i0 + k]);
+  const int i0 = unit_i0(ur.word), nit = unit_nit(ur.word);
+  const int q_row0 = ur.q_row0;
+  const int M = ur.n_cand * p.G;
+  const int ntiles = (int)ur.ntiles;
 
   float m_run[RB], l_run[RB];
   f32x4_t acc[RB][8];
@@ -417,24 +447,32 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i
 #pragma unroll
   for (int e = 0; e < kQPerThread; ++e) {
     const int c = tx + 256 * e, r = c >> 4, ch = c & 15;
-    const uint32_t qoff = r < M ? (uint32_t)global_row(p, it, g, r) * kRowBytes + 16 * ch : 0x80000000u;
+    const uint32_t qoff = r < M ? (uint32_t)global_row(p, q_row0, g, r) * kRowBytes + 16 * ch : 0x80000000u;
     qv[e] = __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff, 0, 0);
   }
+  __builtin_amdgcn_sched_barrier(0);   // the query loads go out before the wait for the first item
   // wave w takes the chain's tiles T = w, w + 4, ...  The first tile's loads
   // are issued unconditionally (a wave without tiles loads through an empty
   // resource, which reads nothing), so the wait for the query rows below
-  // does not have to include them.
+  // does not have to include them.  The first item (slot and flags of the
+  // whole chain) comes with its chunk; a wave whose first tile lies in a
+  // later item of the chain rebuilds its resources from that item.
+  const FirstItem fi = load_first_item(p, ur);
+  const Item &it = fi.it;
   int T = w;
   TileCursor cur;
   NextTile nx;
-  nx.krs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.q), (short)0, 0, kBufferFlags);
-  nx.vrs = nx.krs;
-  nx.tb = 0;
-  if (T < ntiles) {
+  const __amdgpu_buffer_rsrc_t empty =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.q), (short)0, 0, kBufferFlags);
+  const bool has_tile = T < ntiles;
+  nx.krs = has_tile ? item_rsrc_at(p, it, fi.k, fi.hs, g) : empty;
+  nx.vrs = has_tile ? item_rsrc_at(p, it, fi.v, fi.hs, g) : empty;
+  nx.tb = T * kTile;
+  if (has_tile && T >= tiles_of(it)) {
     seek(p, i0, nit, cur, T);
     const Item ic = p.items[i0 + cur.k];
-    nx.krs = item_rsrc(p, ic, g, p.k);
-    nx.vrs = item_rsrc(p, ic, g, p.v);
+    nx.krs = item_rsrc(p, ic, item_chunk(ic), g, p.k);
+    nx.vrs = item_rsrc(p, ic, item_chunk(ic), g, p.v);
     nx.tb = (T - cur.base) * kTile;
   }
   load_kv(nx);
@@ -447,14 +485,14 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i
 
   if (T < ntiles) {
     int tb = nx.tb;
-    int count = p.items[i0 + cur.k].tok_count;
+    int count = cur.k == 0 ? it.tok_count : p.items[i0 + cur.k].tok_count;
     for (; T + kWaves < ntiles; T += kWaves) {
       const int kprev = cur.k;
       seek(p, i0, nit, cur, T + kWaves);
       if (cur.k != kprev) {
         const Item in = p.items[i0 + cur.k];
-        nx.krs = item_rsrc(p, in, g, p.k);
-        nx.vrs = item_rsrc(p, in, g, p.v);
+        nx.krs = item_rsrc(p, in, item_chunk(in), g, p.k);
+        nx.vrs = item_rsrc(p, in, item_chunk(in), g, p.v);
       }
       nx.tb = (T + kWaves - cur.base) * kTile;
       tile(tb, count, std::integral_constant<bool, true>{}, nx);
@@ -482,7 +520,7 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, int i
     }
   }
   __syncthreads();
-  fold_into_slot<RB * 16>(p, it, g, M, tx, aw, mw, lw);
+  fold_into_slot<RB * 16>(p, it, q_row0, g, M, tx, aw, mw, lw);
 }
 
 // ---------------------------------------------------------------------------
@@ -511,16 +549,16 @@ constexpr int kRowsAhead = 4;   // tiles of loads in flight per wave; even, so s
 constexpr int kRowsLdsBytes = 2 * 2 * kTileBytes;  // two K + V tile buffers
 
 template <typename P>
-__device__ __forceinline__ void rows_unit(const P &p, unsigned char *smem, int i0, int nit, int tx, int g) {
+__device__ __forceinline__ void rows_unit(const P &p, unsigned char *smem, const UnitRec &ur, int tx, int g) {
   const int w = __builtin_amdgcn_readfirstlane(tx >> 6);   // wave-uniform
   const int lane = tx & 63;
   const int lr = lane & 15;
   const int lq = lane >> 4;
-  const Item it = p.items[i0];          // request, slot and flags of the whole chain
-  const int M = it.n_cand * p.G;
+  const int i0 = unit_i0(ur.word);
+  const int q_row0 = ur.q_row0;
+  const int M = ur.n_cand * p.G;
   const bool active = 16 * w < M;       // wave-uniform: the wave has rows
-  int ntiles = 0;
-  for (int k = 0; k < nit; ++k) ntiles += tiles_of(p.items[i0 + k]);
+  const int ntiles = (int)ur.ntiles;
 
   const uint32_t stride_b = p.tok_stride * 2;                // bytes between tokens
   const uint32_t voff = (8 * w + lq) * stride_b + 16 * lr;     // token 8w + lq, chunk lr
@@ -531,11 +569,14 @@ __device__ __forceinline__ void rows_unit(const P &p, unsigned char *smem, int i
   const int row = 16 * w + lr;
   const __amdgpu_buffer_rsrc_t qrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t *>(p.q), (short)0, (int)((uint32_t)p.st.R * kRowBytes), kBufferFlags);
-  const uint32_t qoff = row < M ? (uint32_t)global_row(p, it, g, row) * kRowBytes + 16 * lq : 0x80000000u;
+  const uint32_t qoff = row < M ? (uint32_t)global_row(p, q_row0, g, row) * kRowBytes + 16 * lq : 0x80000000u;
   bf16x8_t qop[4];
 #pragma unroll
   for (int s = 0; s < 4; ++s)
     qop[s] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 64 * s, 0, 0));
+  __builtin_amdgcn_sched_barrier(0);   // the query loads go out before the wait for the first item
+  const FirstItem fi = load_first_item(p, ur);   // slot and flags of the whole chain
+  const Item &it = fi.it;
 
   // loads of tile t: K rows 8w + lq and 8w + 4 + lq, then the same V rows.
   // Tiles are requested in order; the resources of the current item are
@@ -546,17 +587,18 @@ __device__ __forceinline__ void rows_unit(const P &p, unsigned char *smem, int i
   // they go through an empty resource.
   const __amdgpu_buffer_rsrc_t empty =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.q), (short)0, 0, kBufferFlags);
-  int lk = 0, lbase = 0, lend = tiles_of(p.items[i0]);
-  __amdgpu_buffer_rsrc_t lkrs = item_rsrc(p, p.items[i0], g, p.k);
-  __amdgpu_buffer_rsrc_t lvrs = item_rsrc(p, p.items[i0], g, p.v);
+  int lk = 0, lbase = 0, lend = tiles_of(it);
+  __amdgpu_buffer_rsrc_t lkrs = item_rsrc_at(p, it, fi.k, fi.hs, g);
+  __amdgpu_buffer_rsrc_t lvrs = item_rsrc_at(p, it, fi.v, fi.hs, g);
   auto issue = [&](u32x4_t (&d)[4], int t) {
     if (t >= lend && t < ntiles) {
       while (t >= lend) {
         lbase = lend;
         lend += tiles_of(p.items[i0 + ++lk]);
       }
-      lkrs = item_rsrc(p, p.items[i0 + lk], g, p.k);
-      lvrs = item_rsrc(p, p.items[i0 + lk], g, p.v);
+      const Item il = p.items[i0 + lk];
+      lkrs = item_rsrc(p, il, item_chunk(il), g, p.k);
+      lvrs = item_rsrc(p, il, item_chunk(il), g, p.v);
     }
     const bool in = t < ntiles;
     const __amdgpu_buffer_rsrc_t krs = in ? lkrs : empty;
@@ -585,7 +627,7 @@ __device__ __forceinline__ void rows_unit(const P &p, unsigned char *smem, int i
   const int vsw = 2 * (vrow & 7);
   const int vc0 = (lr & 3) >> 1;
   // item of the tile being attended: index, first tile, end tile, tokens
-  int ck = 0, cbase = 0, cend = lend, count = p.items[i0].tok_count;
+  int ck = 0, cbase = 0, cend = lend, count = it.tok_count;
 
   // attend staged tile t (tokens [tb, tb + 32) of an item with `count` tokens)
   auto attend = [&](const unsigned char *buf, int t) {
@@ -701,7 +743,7 @@ __device__ __forceinline__ void rows_unit(const P &p, unsigned char *smem, int i
   if (!active) return;
   l_run = xgroup_sum(l_run);
   if (row >= M) return;
-  const size_t idx = (size_t)it.slot * p.st.R + global_row(p, it, g, row);
+  const size_t idx = (size_t)it.slot * p.st.R + global_row(p, q_row0, g, row);
   float *ap = p.st.a + idx * kHeadDim + 4 * lq;
   if (it.flags & kSlotFresh) {
 #pragma unroll
@@ -738,21 +780,23 @@ __device__ __forceinline__ void rows_unit(const P &p, unsigned char *smem, int i
 // reduced over the 16 lanes of a DPP row.
 // ---------------------------------------------------------------------------
 template <int MAXR, typename P>
-__device__ __forceinline__ void valu_unit(const P &p, float *smem, int i0, int nit, int tx, int g) {
+__device__ __forceinline__ void valu_unit(const P &p, float *smem, const UnitRec &ur, int tx, int g) {
   const int w = __builtin_amdgcn_readfirstlane(tx >> 6);   // wave-uniform
   const int lane = tx & 63;
   const int c = lane & 15;
   const int tg = lane >> 4;
-  const Item it = p.items[i0];          // request, slot and flags of the whole chain
-  const int M = it.n_cand * p.G;
-  int ntiles = 0;
-  for (int k = 0; k < nit; ++k) ntiles += tiles_of(p.items[i0 + k]);
+  const int i0 = unit_i0(ur.word), nit = unit_nit(ur.word);
+  const int q_row0 = ur.q_row0;
+  const int M = ur.n_cand * p.G;
+  const int ntiles = (int)ur.ntiles;
+  const FirstItem fi = load_first_item(p, ur);   // slot and flags of the whole chain
+  const Item &it = fi.it;
 
   float qf[MAXR][8];
 #pragma unroll
   for (int r = 0; r < MAXR; ++r) {
     if (r < M) {
-      const u32x4_t q4 = reinterpret_cast<const u32x4_t *>(p.q + (size_t)global_row(p, it, g, r) * kHeadDim)[c];
+      const u32x4_t q4 = reinterpret_cast<const u32x4_t *>(p.q + (size_t)global_row(p, q_row0, g, r) * kHeadDim)[c];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         qf[r][2 * e] = bf16_lo(q4[e]);
@@ -852,24 +896,27 @@ __device__ __forceinline__ void valu_unit(const P &p, float *smem, int i0, int n
   if (T < ntiles) {
     TileCursor cur;
     NextTile nx;
-    seek(p, i0, nit, cur, T);
-    {
+    nx.krs = item_rsrc_at(p, it, fi.k, fi.hs, g);
+    nx.vrs = item_rsrc_at(p, it, fi.v, fi.hs, g);
+    nx.tb = T * kTile;
+    if (T >= tiles_of(it)) {
+      seek(p, i0, nit, cur, T);
       const Item ic = p.items[i0 + cur.k];
-      nx.krs = item_rsrc(p, ic, g, p.k);
-      nx.vrs = item_rsrc(p, ic, g, p.v);
+      nx.krs = item_rsrc(p, ic, item_chunk(ic), g, p.k);
+      nx.vrs = item_rsrc(p, ic, item_chunk(ic), g, p.v);
       nx.tb = (T - cur.base) * kTile;
     }
     load_k(nx);
     load_v(nx);
     int tb = nx.tb;
-    int count = p.items[i0 + cur.k].tok_count;
+    int count = cur.k == 0 ? it.tok_count : p.items[i0 + cur.k].tok_count;
     for (; T + kWaves < ntiles; T += kWaves) {
       const int kprev = cur.k;
       seek(p, i0, nit, cur, T + kWaves);
       if (cur.k != kprev) {
         const Item in = p.items[i0 + cur.k];
-        nx.krs = item_rsrc(p, in, g, p.k);
-        nx.vrs = item_rsrc(p, in, g, p.v);
+        nx.krs = item_rsrc(p, in, item_chunk(in), g, p.k);
+        nx.vrs = item_rsrc(p, in, item_chunk(in), g, p.v);
       }
       nx.tb = (T + kWaves - cur.base) * kTile;
       tile(tb, count, std::integral_constant<bool, true>{}, nx);
@@ -902,7 +949,7 @@ __device__ __forceinline__ void valu_unit(const P &p, float *smem, int i0, int n
     }
   }
   __syncthreads();
-  fold_into_slot<MAXR>(p, it, g, M, tx, aw, mw, lw);
+  fold_into_slot<MAXR>(p, it, q_row0, g, M, tx, aw, mw, lw);
 }
 
 constexpr int kValuLdsBytes = kWaves * kMaxValuRows * (kAwPitch + 2) * 4;
@@ -911,15 +958,19 @@ static_assert(MfmaLds<1>::kBytes <= kChunkLdsBytes, "LDS sizes");
 static_assert(kRowsLdsBytes <= kChunkLdsBytes && 2 * kChunkLdsBytes <= 160 * 1024, "LDS sizes");
 
 // ---------------------------------------------------------------------------
-// History kernel: one launch for every unit of a call.  Workgroup =
-// (kv head, w) = (blockIdx.x, blockIdx.y) first attends the units of its own
-// list in order (the host gives every workgroup an equal share of the
-// call's tokens, which may span several requests); each unit's kind selects
-// the body: MFMA with two or one 16-row blocks, the row-split body for
-// three or four (only on the wide instantiation, which a launch with such a
-// unit runs on), or the VALU path for <= 4 rows (built for 1, 2 and 4 rows).  The heads are the fast grid dimension:
-// with 8 KV heads the round-robin placement gives every XCD one head of
-// every workgroup's share.
+// History kernel: one launch for every unit of a call.  Workgroup w of KV
+// head g first attends the units of its own list in order (the host gives
+// every workgroup an equal share of the call's tokens, which may span
+// several requests); each unit's kind selects the body: MFMA with two or
+// one 16-row blocks, the row-split body for three or four (only on the wide
+// instantiation, which a launch with such a unit runs on), or the VALU path
+// for <= 4 rows (built for 1, 2 and 4 rows).  The grid is (g, w) with the
+// heads as the fast dimension for token-major chunks, where the eight XCDs
+// then read the eight heads of the same tokens, and (w, g) for head-major
+// chunks, where every XCD then reads every head's plane: on MI355X a
+// head-major launch over 16 x 32768 tokens took 354 us with the heads fast
+// and 323 us the other way round (the same box; a loads-only copy of the
+// kernel 347 against 318 us, and a plain read of the same 2 GiB 301 us).
 //
 // The XCDs do not stream at the same rate (on MI355X some finish an equal
 // share 10% later than others), so the host may hold back the last part of
@@ -938,21 +989,30 @@ template <bool Wide, typename P>
 __global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[kChunkLdsBytes];
   __shared__ uint32_t claim_sh;
-  const int u0 = p.wg_first[blockIdx.y];
-  const int u1 = p.wg_first[blockIdx.y + 1];
+  const int y = p.heads_fast ? blockIdx.y : blockIdx.x;     // workgroup of its KV head
+  const int g_own = p.heads_fast ? blockIdx.x : blockIdx.y;  // KV head of its own units
+  // The workgroup's first unit record and the range of its further units
+  // are read together at the start and forced into registers here, so
+  // neither the first unit's loads nor its end wait for a second round of
+  // argument reads.
+  UnitRec ur = p.units[y];
+  uint32_t more0 = p.more[y], more1 = p.more[y + 1];
+  asm volatile("" : "+s"(ur.word), "+s"(ur.ntiles), "+s"(ur.q_row0), "+s"(ur.n_cand), "+s"(more0), "+s"(more1));
   const uint32_t nclaims = (uint32_t)p.num_tail * (uint32_t)p.Hkv;
   const uint32_t last_claim = nclaims + (uint32_t)p.Hkv * (uint32_t)p.num_wgs - 1u;
-  int u = u0;
+  uint32_t u = more0;
   bool first = true;
   for (;;) {
-    int uidx, g;
-    if (u < u1) {
-      if (!first) __syncthreads();   // the previous unit's fold has read the LDS this unit restages
-      uidx = u++;
-      g = blockIdx.x;
+    int g = g_own;
+    if (first) {
+      first = false;
+      if (unit_nit(ur.word) == 0) continue;   // a workgroup without units of its own
+    } else if (u < more1) {
+      __syncthreads();   // the previous unit's fold has read the LDS this unit restages
+      ur = p.units[u++];
     } else {
       if (nclaims == 0) break;
-      if (!first) __syncthreads();   // ... and every thread has read the previous claim
+      __syncthreads();   // ... and every thread has read the previous claim
       if (threadIdx.x == 0) {
         const uint32_t c = atomicAdd(p.claim, 1u);
         if (c == last_claim) __hip_atomic_store(p.claim, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -962,41 +1022,37 @@ __global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
       const uint32_t c = __builtin_amdgcn_readfirstlane(claim_sh);
       if (c >= nclaims) break;
       const uint32_t t = c / (uint32_t)p.Hkv;
-      uidx = p.tail_first + (int)t;
+      ur = p.units[p.tail_first + (int)t];
       g = (int)(c - t * (uint32_t)p.Hkv);
     }
-    first = false;
     // The bodies derive their per-lane addresses from tx.  Passing it
     // through an empty asm each unit keeps the compiler from computing
     // them once before the loop and holding all three bodies' worth live
     // across it (that spilled 14 registers and cost 6% on one-unit calls).
     int tx = threadIdx.x;
     asm volatile("" : "+v"(tx));
-    const uint32_t unit = p.units[uidx];
-    const int i0 = unit & 0xffff;
-    const int nit = (unit >> 16) & 0xff;
-    const int kind = unit >> 24;
+    const int kind = unit_kind(ur.word);
     if constexpr (Wide) {
       if (kind >= kUnitMfma3) {
-        rows_unit(p, smem, i0, nit, tx, g);
+        rows_unit(p, smem, ur, tx, g);
         continue;
       }
     }
     if (kind == kUnitMfma2)
-      mfma_unit<2>(p, smem, i0, nit, tx, g);
+      mfma_unit<2>(p, smem, ur, tx, g);
     else if (kind == kUnitMfma1)
-      mfma_unit<1>(p, smem, i0, nit, tx, g);
+      mfma_unit<1>(p, smem, ur, tx, g);
     else {
       // the VALU body's work grows with the rows it is built for: build it
       // for 1, 2 and 4 rows and take the smallest that holds the unit
-      const int rows = p.items[i0].n_cand * p.G;
+      const int rows = ur.n_cand * p.G;
       float *lds = reinterpret_cast<float *>(smem);
       if (rows <= 1)
-        valu_unit<1>(p, lds, i0, nit, tx, g);
+        valu_unit<1>(p, lds, ur, tx, g);
       else if (rows <= 2)
-        valu_unit<2>(p, lds, i0, nit, tx, g);
+        valu_unit<2>(p, lds, ur, tx, g);
       else
-        valu_unit<kMaxValuRows>(p, lds, i0, nit, tx, g);
+        valu_unit<kMaxValuRows>(p, lds, ur, tx, g);
     }
   }
 }
@@ -1169,10 +1225,11 @@ template <bool Wide, typename D>
 hipError_t launch_chunk_as(const ChunkParams &p, hipStream_t s) {
   static thread_local D d;
   static_cast<ChunkHeader &>(d) = p;
-  std::memcpy(d.units, p.units, sizeof(uint32_t) * p.num_units);
-  std::memcpy(d.wg_first, p.wg_first, sizeof(uint16_t) * (p.num_wgs + 1));
+  std::memcpy(d.units, p.units, sizeof(UnitRec) * p.num_units);
+  std::memcpy(d.more, p.more, sizeof(uint32_t) * (p.num_wgs + 1));
   std::memcpy(d.items, p.items, sizeof(Item) * p.num_items);
-  hipLaunchKernelGGL((chunk_attn<Wide, D>), dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, d);
+  const dim3 grid = p.heads_fast ? dim3(p.Hkv, p.num_wgs) : dim3(p.num_wgs, p.Hkv);
+  hipLaunchKernelGGL((chunk_attn<Wide, D>), grid, dim3(256), 0, s, d);
   return hipGetLastError();
 }
 
@@ -1183,7 +1240,8 @@ hipError_t launch_chunk_sized(const ChunkParams &p, hipStream_t s) {
   };
   if (fits(ChunkSmall::kUnits, ChunkSmall::kItems, ChunkSmall::kWgs)) return launch_chunk_as<Wide, ChunkSmall>(p, s);
   if (fits(ChunkMedium::kUnits, ChunkMedium::kItems, ChunkMedium::kWgs)) return launch_chunk_as<Wide, ChunkMedium>(p, s);
-  hipLaunchKernelGGL((chunk_attn<Wide, ChunkParams>), dim3(p.Hkv, p.num_wgs), dim3(256), 0, s, p);
+  const dim3 grid = p.heads_fast ? dim3(p.Hkv, p.num_wgs) : dim3(p.num_wgs, p.Hkv);
+  hipLaunchKernelGGL((chunk_attn<Wide, ChunkParams>), grid, dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
@@ -1192,7 +1250,7 @@ hipError_t launch_chunk_sized(const ChunkParams &p, hipStream_t s) {
 hipError_t launch_chunk(const ChunkParams &p, hipStream_t s) {
   // a launch with any unit of more than two 16-row blocks runs on the wide kernel
   for (int u = 0; u < p.num_units; ++u)
-    if ((int)(p.units[u] >> 24) >= kUnitMfma3) return launch_chunk_sized<true>(p, s);
+    if (unit_kind(p.units[u].word) >= kUnitMfma3) return launch_chunk_sized<true>(p, s);
   return launch_chunk_sized<false>(p, s);
 }
 

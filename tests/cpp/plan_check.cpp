@@ -21,10 +21,11 @@
 
 namespace {
 struct Rec {
-  std::vector<ss::Item> items; std::vector<uint32_t> units; std::vector<uint16_t> wg_first; int kind;
+  std::vector<ss::Item> items; std::vector<uint32_t> units; std::vector<uint32_t> wg_first; int kind;
   int tail_first, num_tail; uint32_t *claim; int clears_before; int Hkv;
 };
 int g_finalize_launches = 0;
+long g_empty_wgs = 0;             // workgroups launched without a unit of their own
 int g_clear_n = 0;
 std::vector<Rec> g_recs;
 const ss::ChunkParams *g_last = nullptr;
@@ -33,16 +34,47 @@ uint32_t *g_clear_ptr = nullptr;
 }
 
 namespace ss {
+// Record a launch.  The unit records are checked against the items they
+// name, then flattened into the order the kernel attends them: workgroup w's
+// first unit (record w, unless empty), its further units [more[w],
+// more[w + 1]), ..., then the tail; the tables below use that order, with
+// unit words (i0 | nit << 16 | kind << 24).
 static void rec(const ChunkParams &p, int kind) {
   Rec r;
   r.items.assign(p.items, p.items + p.num_items);
-  r.units.assign(p.units, p.units + p.num_units);
-  r.wg_first.assign(p.wg_first, p.wg_first + p.num_wgs + 1);
   if (p.num_wgs < 1 || p.num_wgs > kMaxWgs) { printf("bad workgroup count\n"); exit(1); }
+  if (p.num_units < p.num_wgs || p.num_units > kMaxUnits || p.num_items < 1 || p.num_items > kMaxItems) { printf("bad counts\n"); exit(1); }
+  const int W = p.num_wgs;
+  const int tail_first = p.num_tail > 0 ? p.tail_first : p.num_units;
+  bool ok = p.more[0] == (uint32_t)W && p.more[W] == (uint32_t)tail_first &&
+            tail_first + (p.num_tail > 0 ? p.num_tail : 0) == p.num_units;
+  for (int w = 0; w < W; ++w) ok = ok && p.more[w] <= p.more[w + 1];
+  if (!ok) { printf("bad unit ranges\n"); exit(1); }
+  auto word = [&](int u) {
+    const UnitRec &ur = p.units[u];
+    const int i0 = unit_i0(ur.word), nit = unit_nit(ur.word);
+    if (nit < 1 || i0 + nit > p.num_items) { printf("unit %d: items [%d, +%d) outside the table\n", u, i0, nit); exit(1); }
+    uint32_t tiles = 0;
+    for (int i = i0; i < i0 + nit; ++i) tiles += (uint32_t)((p.items[i].tok_count + kTile - 1) / kTile);
+    const Item &it = p.items[i0];
+    if (ur.ntiles != tiles || ur.q_row0 != it.q_row0 || ur.n_cand != it.n_cand || unit_chunk(ur.word) != it.chunk) {
+      printf("unit %d: record does not match its items\n", u);
+      exit(1);
+    }
+    return (uint32_t)i0 | ((uint32_t)nit << 16) | ((uint32_t)unit_kind(ur.word) << 24);
+  };
+  for (int w = 0; w < W; ++w) {
+    r.wg_first.push_back((uint16_t)r.units.size());
+    if (unit_nit(p.units[w].word) > 0) r.units.push_back(word(w));
+    else g_empty_wgs++;
+    for (uint32_t u = p.more[w]; u < p.more[w + 1]; ++u) r.units.push_back(word((int)u));
+  }
+  r.wg_first.push_back((uint16_t)r.units.size());
+  r.tail_first = (int)r.units.size();
+  for (int u = tail_first; u < p.num_units; ++u) r.units.push_back(word(u));
   r.kind = kind;
-  r.tail_first = p.tail_first; r.num_tail = p.num_tail; r.claim = p.claim; r.clears_before = g_clears;
+  r.num_tail = p.num_tail; r.claim = p.claim; r.clears_before = g_clears;
   r.Hkv = p.Hkv;
-  if (p.num_units < 1 || p.num_units > kMaxUnits || p.num_items < 1 || p.num_items > kMaxItems) { printf("bad counts\n"); exit(1); }
   g_recs.push_back(r);
   g_last = &p;
 }
@@ -315,6 +347,9 @@ int main() {
     scenario("config1 split 32", 1, 8, 2, {5}, {4096}, 1024, 32, layout, 1);
     scenario("config1 split 96", 1, 8, 2, {5}, {4096}, 1024, 96, layout, 1);
     scenario("config1 batched", 1, 8, 2, {5}, {4096}, 1024, 0, layout, 4);
+    // shares of 16.5 tokens: the first share ends below the first tile boundary, so workgroup 0 has no unit
+    scenario("33 tokens, split 32 (a workgroup without units)", 1, 8, 2, {5}, {33}, 64, 32, layout, 1);
+    scenario("ragged, split 32 (workgroups without units)", 3, 32, 8, {2, 7, 1}, {33, 97, 65}, 64, 32, layout, 2);
     scenario("config2 per-chunk", 1, 32, 8, {5}, {16384}, 2048, 0, layout, 1);
     // one workgroup per CU: 8 KV heads x 32
     scenario("config3 batched 8", 16, 32, 8, std::vector<int>(16, 6), std::vector<int>(16, 32768), 4096, 0, layout, 8, 0, 0, 1, 32);
@@ -364,6 +399,8 @@ int main() {
       scenario(nm, B, hq, hkv, nc, h, S, split, layout, batch, (int)(rng() % 6), bal);
     }
   }
+  printf("workgroups without units of their own: %ld\n", g_empty_wgs);
+  CHECK(g_empty_wgs > 0, "no launch had a workgroup without units of its own");
   printf("%s\n", fails ? "FAILURES" : "all ok");
   return fails ? 1 : 0;
 }
