@@ -7,7 +7,8 @@ attended in one batched call, the Speculative Frontier call and finalize, on
 one HIP stream: two kernel launches per round (the workspace is zero-filled
 once and reused with counters_zeroed, so no counter clear runs per round).
 Workload: 16 requests x 32768 history tokens, 32 query / 8 KV heads, d = 128,
-6 candidate queries per request, bf16 synthetic inputs (seeded, N(0,1)-like).
+6 candidate queries per request, bf16 synthetic inputs (seeded, N(0,1)-like);
+each chunk is head-major with a token's K and V rows adjacent, [Hkv][tok][2][d].
 
 value = algorithmic KV bytes per round (sum_b (C_b + n_b) * Hkv * d * 2 * 2)
         x steps / device time of the timed steps.
@@ -579,9 +580,10 @@ def main() -> int:
     ap.add_argument("--batch", type=int, default=0,
                     help="history chunks per history call in the timed round "
                          "(0 = all resident chunks in one call, 1 = one call per chunk)")
-    ap.add_argument("--kv-layout", choices=["token", "head", "head-kv"], default="head",
+    ap.add_argument("--kv-layout", choices=["token", "head", "head-kv"], default="head-kv",
                     help="history chunk layout: token-major [tok][Hkv][d], head-major [Hkv][tok][d] or "
-                         "head-major with each token's K and V rows adjacent [Hkv][tok][2][d]")
+                         "head-major with each token's K and V rows adjacent [Hkv][tok][2][d] (the default: "
+                         "one contiguous stream per KV head, measured 0.5-3%% faster than head-major)")
     ap.add_argument("--balance-permille", type=int, default=0,
                     help="ss_round_desc.balance_permille: share of each workgroup's tokens left to the "
                          "cross-die balancing tail (0 = the library's default, -1 = no tail)")
@@ -724,7 +726,8 @@ def main() -> int:
     if os.path.exists(TRAFFIC_FILE):
         try:
             tr = json.load(open(TRAFFIC_FILE))
-            if tr.get("kernel_code_sha256_16") == kernel_source_hash() and tr.get("config") == args.config:
+            if (tr.get("kernel_code_sha256_16") == kernel_source_hash() and tr.get("config") == args.config
+                    and tr.get("kv_layout") == args.kv_layout):
                 traffic = tr.get("hbm_bytes_per_launch")
         except Exception:
             traffic = None
