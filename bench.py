@@ -15,7 +15,8 @@ value = algorithmic KV bytes per round (sum_b (C_b + n_b) * Hkv * d * 2 * 2)
 
 Order of the run: input generation; 60 rounds in blocks of 10 (`transient`:
 the GPU's power management slows HBM-bound rounds for a few milliseconds
-after it starts streaming, then settles); a device-to-device copy probe; the
+after it starts streaming, then settles); a device-to-device copy probe and a
+plain read of 2 GiB (the HBM ceilings, on the settled GPU), then 20 rounds; the
 per-launch timing of the round's kernel (`roofline`); per-round percentiles;
 the W warm-up and K timed rounds (`value`); then the secondary measurements.
 
@@ -103,11 +104,15 @@ def transient_blocks(torch, H, b, chunks, stream, blocks: int, per_block: int, b
     return [round(e0.elapsed_time(e1) * 1e3 / per_block, 2) for e0, e1 in evs]
 
 
-def copy_probe(torch, stream, nbytes: int = 1 << 31, reps: int = 5):
+def copy_probe(torch, stream, nbytes: int = 1 << 31, reps: int = 5, bufs=None):
     """HBM ceiling check: a plain device-to-device copy of `nbytes` (torch's
-    copy kernel), timed with HIP events; GB/s counts bytes read plus written."""
-    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
-    dst = torch.empty_like(src)
+    copy kernel), timed with HIP events; GB/s counts bytes read plus written.
+    `bufs` = (src, dst) of at least `nbytes` each, else allocated here."""
+    if bufs is None:
+        src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+    else:
+        src, dst = bufs[0][:nbytes], bufs[1][:nbytes]
     with torch.cuda.stream(stream):
         dst.copy_(src)
         ts = []
@@ -121,7 +126,8 @@ def copy_probe(torch, stream, nbytes: int = 1 << 31, reps: int = 5):
     torch.cuda.synchronize()
     t = sorted(e0.elapsed_time(e1) / 1e3 for e0, e1 in ts)
     del src, dst
-    torch.cuda.empty_cache()
+    if bufs is None:
+        torch.cuda.empty_cache()
     med = t[len(t) // 2]
     return {"bytes_copied": nbytes, "median_ms": round(med * 1e3, 3),
             "GBs_read_plus_written": round(2 * nbytes / med / 1e9, 1),
@@ -129,12 +135,13 @@ def copy_probe(torch, stream, nbytes: int = 1 << 31, reps: int = 5):
 
 
 def read_probe(torch, ss, stream, nbytes: int = 1 << 31, reps: int = 7, grids=(256, 512, 1024, 2048, 4096),
-               settle: int = 100):
+               settle: int = 100, buf=None):
     """Read ceiling: ss_probe_read streams `nbytes` of HBM with the history
     kernel's load form (16 B per lane, non-temporal, 8 loads in flight per
     lane) and nothing else, over each grid size, after `settle` untimed
     reads; GB/s of the best grid's median (HIP events on `stream`)."""
-    buf = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    own = buf is None
+    buf = torch.ones(nbytes, dtype=torch.uint8, device="cuda") if own else buf[:nbytes]
     sink = torch.empty(max(grids), dtype=torch.int32, device="cuda")
     res = {}
     with torch.cuda.stream(stream):
@@ -156,7 +163,8 @@ def read_probe(torch, ss, stream, nbytes: int = 1 << 31, reps: int = 7, grids=(2
             t = sorted(e0.elapsed_time(e1) / 1e3 for e0, e1 in ts)
             res[str(g)] = round(nbytes / t[len(t) // 2] / 1e9, 1)
     del buf, sink
-    torch.cuda.empty_cache()
+    if own:
+        torch.cuda.empty_cache()
     best = max(res, key=res.get)
     return {"bytes_read": nbytes, "GBs": res[best], "workgroups": int(best), "GBs_by_workgroups": res}
 
@@ -650,11 +658,12 @@ def main() -> int:
                      num_q_heads=args.num_q_heads or w.num_q_heads, num_kv_heads=w.num_kv_heads,
                      head_dim=w.head_dim, chunk_tokens=w.chunk_tokens, cfg_id=args.config)
     probe = read = None
+    probe_bufs = None
     if not (args.streamed_trace or args.streamed_only or args.per_launch_only):
-        # HBM ceilings first: freeing the probes' buffers stalls the next launches for tens of ms
-        log("bench: device-to-device copy probe and read probe")
-        probe = copy_probe(torch, torch.cuda.Stream())
-        read = read_probe(torch, ss, torch.cuda.Stream())
+        # the HBM ceilings are measured after the settling rounds, on buffers allocated here (allocating or
+        # freeing them later would stall the launches around it)
+        probe_bufs = (torch.ones(1 << 31, dtype=torch.uint8, device="cuda"),
+                      torch.empty(1 << 31, dtype=torch.uint8, device="cuda"))
     log(f"bench: config {args.config} ({w.name}): generating inputs on the GPU")
     if args.streamed_trace:
         b = H.RoundBuffers(w, kv_layout=layout, balance_permille=args.balance_permille)
@@ -693,6 +702,11 @@ def main() -> int:
 
     log("bench: rounds right after the input generation, blocks of 10")
     transient = transient_blocks(torch, H, b, chunks, stream, 6, 10, batch)
+    # HBM ceilings on the settled GPU: a device-to-device copy and a plain read of 2 GiB
+    log("bench: device-to-device copy probe and read probe")
+    probe = copy_probe(torch, stream, bufs=probe_bufs)
+    read = read_probe(torch, ss, stream, buf=probe_bufs[0])
+    transient_blocks(torch, H, b, chunks, stream, 2, 10, batch)   # the round again after the probes
     log("bench: per-launch timing of the round's kernel")
     times = per_launch_times(torch, ss, b, chunks, stream, 5, batch)
     big = max(nb for _, nb in times)
@@ -708,6 +722,7 @@ def main() -> int:
     kv_bytes = w.algorithmic_kv_bytes()
     value = kv_bytes * args.steps / dt / 1e9
     out_gpu, lse_gpu = b.out.clone(), b.lse.clone()
+    probe_bufs = None   # freed after the timed rounds
 
     per_chunk = None
     if batch != 1:
