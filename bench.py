@@ -22,10 +22,11 @@ the W warm-up and K timed rounds (`value`); then the secondary measurements.
 
 Extra objects on the JSON line:
   roofline      the round's dominant kernel (the history attention launch):
-                algorithmic bytes per launch / mean launch time (HIP events
-                on its stream), vs 8 TB/s and vs the copy probe's measured
-                rate; HBM traffic from committed rocprofv3 counter runs if
-                the kernel source still matches them
+                algorithmic bytes per launch / mean launch time (launches
+                back to back between HIP events on their stream), vs 8 TB/s
+                and vs the copy and read probes' measured rates; HBM traffic
+                from committed rocprofv3 counter runs if the kernel source
+                and chunk layout still match them
   cpu_baseline  the fp64 oracle timed on this host's cores on the same
                 workload; `parity` compares its output with the GPU round's
   streamed      the same round with the history streamed from pinned host
@@ -200,6 +201,33 @@ def per_launch_times(torch, ss, b, chunks, stream, rounds: int, batch: int):
         for e0, e1, nbytes in evs:
             times.append((e0.elapsed_time(e1) / 1e3, nbytes))
     return times
+
+
+def b2b_launch_time(torch, ss, b, chunks, stream, rounds: int, batch: int, blocks: int = 3):
+    """Mean duration of the round's history launches run back to back: per
+    block, `rounds` rounds of only init and the history calls (no frontier
+    call or finalize; the handle is destroyed unfinalized), between two HIP
+    events on the launch stream; the median block.  One pair of events per
+    block keeps the events' own cost out of the figure."""
+    w = b.w
+    groups = [list(range(i0, min(len(chunks), i0 + batch))) for i0 in range(0, len(chunks), batch)]
+    args = [([chunks[j][0].data_ptr() for j in g], [chunks[j][1].data_ptr() for j in g], [w.chunk_lens(j) for j in g])
+            for g in groups]
+    res = []
+    for _ in range(blocks):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(rounds):
+            r = ss.ss_round_init(b.desc, b.q.data_ptr(), b.ws.data_ptr(), b.ws_bytes, stream.cuda_stream)
+            for ks, vs, ls in args:
+                ss.ss_attend_history_chunks(r, ks, vs, ls, None, None, stream.cuda_stream)
+            ss.ss_round_destroy(r)
+        e1.record(stream)
+        res.append((e0, e1))
+    torch.cuda.synchronize()
+    per = sorted(e0.elapsed_time(e1) / 1e3 / (rounds * len(groups)) for e0, e1 in res)
+    return per[len(per) // 2]
 
 
 def cpu_baseline(w, chunks, sample_requests, gpu_out=None, gpu_lse=None):
@@ -711,8 +739,11 @@ def main() -> int:
     times = per_launch_times(torch, ss, b, chunks, stream, 5, batch)
     big = max(nb for _, nb in times)
     full = [t for t, nb in times if nb == big]
-    launch_s = sum(full) / len(full)
+    single_s = sum(full) / len(full)
     bytes_per_launch = big
+    even = all(sum(sum(w.chunk_lens(j)) for j in range(i0, min(w.num_chunks, i0 + batch))) * w.token_bytes() == big
+               for i0 in range(0, w.num_chunks, batch))
+    launch_s = b2b_launch_time(torch, ss, b, chunks, stream, 10, batch) if even else single_s
     achieved = bytes_per_launch / launch_s / 1e9
     per_round = round_times(torch, H, b, chunks, stream, max(20, args.steps), batch)
 
@@ -730,12 +761,14 @@ def main() -> int:
         dt1, _ = time_round_steps(torch, H, b, chunks, stream, args.steps, 5, 1)
         t1 = per_launch_times(torch, ss, b, chunks, stream, 3, 1)
         big1 = max(nb for _, nb in t1)
-        l1 = [t for t, nb in t1 if nb == big1]
+        even1 = all(sum(w.chunk_lens(j)) * w.token_bytes() == big1 for j in range(w.num_chunks))
+        l1 = b2b_launch_time(torch, ss, b, chunks, stream, 10, 1) if even1 else \
+            sum(t for t, nb in t1 if nb == big1) / len([t for t, nb in t1 if nb == big1])
         per_chunk = {"round_ms": round(dt1 / args.steps * 1e3, 4),
                      "effective_KV_GBs": round(kv_bytes * args.steps / dt1 / 1e9, 2),
                      "pct_of_hbm_peak": round(100.0 * kv_bytes * args.steps / dt1 / 1e9 / HBM_PEAK_GBS, 2),
-                     "mean_launch_us": round(sum(l1) / len(l1) * 1e6, 2),
-                     "launch_GBs": round(big1 / (sum(l1) / len(l1)) / 1e9, 2)}
+                     "mean_launch_us": round(l1 * 1e6, 2),
+                     "launch_GBs": round(big1 / l1 / 1e9, 2)}
 
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
@@ -786,6 +819,10 @@ def main() -> int:
             "traffic": traffic,
             "bytes_per_launch": bytes_per_launch,
             "mean_launch_us": round(launch_s * 1e6, 2),
+            "launch_timing": ("history launches back to back (init and history calls only), 3 blocks of 10 rounds "
+                              "between HIP events on the launch stream, median block" if even else
+                              "HIP events around each history launch"),
+            "mean_launch_us_events_around_each": round(single_s * 1e6, 2),
             "launches_timed": len(full),
             "measured_copy_GBs": copy_gbs,
             "frac_of_measured_copy": round(achieved / copy_gbs, 4),
