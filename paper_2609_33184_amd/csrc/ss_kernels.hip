@@ -12,8 +12,8 @@
 //   * all accumulation is fp32.  In the MFMA path the softmax weights P
 //     (fp32) are split into bf16 hi + lo parts and both are multiplied with V
 //     (two bf16 MFMAs), which keeps P to ~2^-16 relative; rounding P once to
-//     bf16 would cost ~1.6e-3 relative L2 error.  The denominator l is summed
-//     from the same hi + lo values, so numerator and denominator agree.
+//     bf16 would cost ~1.6e-3 relative L2 error.  The denominator l sums the
+//     fp32 weights themselves, which hi + lo carry to that precision.
 //   * a running state is split into kNumSlots slots per query row so that
 //     several workgroups can fold disjoint token ranges of one chunk into the
 //     same row without atomics; the finalize kernel merges the slots.
@@ -384,35 +384,51 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, const
     bf16x8_t phi[RB], plo[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
+      // raw scores up to the exponent (sigma log2(e) > 0 commutes with the
+      // maximum); only an item's last, partial tile needs the token mask
       float x[8];
       float mx = kNegInf;
+      if (tb + kTile <= count) {
 #pragma unroll
-      for (int u = 0; u < 2; ++u)
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = tb + 16 * u + 4 * lq + r;
-          const float v = t < count ? sacc[u][rb][r] * sl2 : kNegInf;
-          x[4 * u + r] = v;
-          mx = fmaxf(mx, v);
-        }
-      mx = xgroup_max(mx);
-      const float mn = fmaxf(m_run[rb], mx);
-      const float alpha = exp2_fast(m_run[rb] - mn);
-      m_run[rb] = mn;
+          for (int r = 0; r < 4; ++r) {
+            x[4 * u + r] = sacc[u][rb][r];
+            mx = fmaxf(mx, sacc[u][rb][r]);
+          }
+      } else {
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = tb + 16 * u + 4 * lq + r;
+            const float v = t < count ? sacc[u][rb][r] : kNegInf;
+            x[4 * u + r] = v;
+            mx = fmaxf(mx, v);
+          }
+      }
+      const float mn = fmaxf(m_run[rb], xgroup_max(mx) * sl2);
+      // Eq. 14's rescale, only when some row's maximum rose (elsewhere the
+      // factor is exactly 1)
+      if (__builtin_amdgcn_ballot_w64(mn > m_run[rb])) {
+        const float alpha = exp2_fast(m_run[rb] - mn);
+        l_run[rb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < 8; ++db) acc[rb][db] *= alpha;
+        m_run[rb] = mn;
+      }
       float ls = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float pe = exp2_fast(x[e] - mn);
+        const float pe = exp2_fast(__builtin_fmaf(x[e], sl2, -mn));
         const __bf16 h = (__bf16)pe;
         const float hf = (float)h;
         const __bf16 lo = (__bf16)(pe - hf);
         phi[rb][e] = h;
         plo[rb][e] = lo;
-        ls += hf + (float)lo;
+        ls += pe;
       }
-      l_run[rb] = alpha * l_run[rb] + ls;
-#pragma unroll
-      for (int db = 0; db < 8; ++db) acc[rb][db] *= alpha;
+      l_run[rb] += ls;
     }
 
     __builtin_amdgcn_sched_barrier(0);
@@ -710,7 +726,7 @@ __device__ __forceinline__ void rows_unit(const P &p, unsigned char *smem, const
       const __bf16 lo = (__bf16)(pe - hf);
       phi[e] = h;
       plo[e] = lo;
-      ls += hf + (float)lo;
+      ls += pe;
     }
     l_run += ls;
 
