@@ -121,3 +121,51 @@ def test_random_round(stream, k):
     assert_parity(outs[0][1].double().cpu().numpy(), ref_l, f"random {k} lse", max_abs=1e-3, rel_l2=1e-4)
     assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1]), \
         f"random {k}: the second round on the same workspace differs"
+
+
+def capacity_case(name: str):
+    """Cohorts whose history launches overflow the smaller kernel-argument
+    tables: more than 64 requests (finalize's larger item table), more than
+    512 units, 1024 items or 256 workgroups per KV head (the largest chunk
+    table), and the same with 64 rows per KV head (the wide kernel's
+    medium and largest tables)."""
+    rng = np.random.default_rng({"req100_split32": 1, "req100_batched": 2, "req300_split96": 3,
+                                 "wide100_split32": 4, "wide100_auto": 5}[name])
+    if name.startswith("req100"):
+        B, hq, hkv, S, layout = 100, 8, 2, 256, ss.SS_KV_TOKEN_MAJOR
+        cands = rng.integers(1, 9, B)
+        lens = rng.integers(0, 601, B)
+        split, batch = (32, 3) if name == "req100_split32" else (0, 3)
+    elif name == "req300_split96":
+        B, hq, hkv, S, layout = 300, 8, 2, 512, ss.SS_KV_HEAD_MAJOR_KV
+        cands = rng.integers(1, 5, B)
+        lens = rng.integers(100, 401, B)
+        split, batch = 96, 1
+    else:
+        B, hq, hkv, S, layout = 100, 64, 8, 1024, ss.SS_KV_HEAD_MAJOR_KV
+        cands = np.full(B, 8)
+        lens = rng.integers(100, 701, B)
+        split, batch = (32 if name == "wide100_split32" else 0), 1
+    return dict(B=B, hq=hq, hkv=hkv, S=S, layout=layout, cands=[int(x) for x in cands],
+                lens=[int(x) for x in lens], split=split, batch=batch)
+
+
+CAPACITY_CASES = ["req100_split32", "req100_batched", "req300_split96", "wide100_split32", "wide100_auto"]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", CAPACITY_CASES)
+def test_table_capacities(stream, name):
+    c = capacity_case(name)
+    w = W.custom(c["lens"], c["cands"], num_q_heads=c["hq"], num_kv_heads=c["hkv"], chunk_tokens=c["S"],
+                 seed_base=77)
+    print(f"capacity case {name}: B={c['B']} {c['hq']}q/{c['hkv']}kv chunks={w.num_chunks} split={c['split']} "
+          f"batch={c['batch']} layout={c['layout']}", flush=True)
+    b = H.RoundBuffers(w, split_tokens=c["split"], kv_layout=c["layout"])
+    chunks = H.hbm_history(w, kv_layout=c["layout"])
+    torch.cuda.synchronize()
+    H.run_round(b, chunks, stream.cuda_stream, batch=c["batch"])
+    stream.synchronize()
+    ref_o, ref_l = oracle_full(w)
+    assert_parity(b.out.double().cpu().numpy(), ref_o, f"capacity {name}")
+    assert_parity(b.lse.double().cpu().numpy(), ref_l, f"capacity {name} lse", max_abs=1e-3, rel_l2=1e-4)
