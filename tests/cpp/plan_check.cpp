@@ -222,7 +222,8 @@ static void check_call(int B, int Hq, int Hkv, const std::vector<int> &ncand, co
       for (int bb = 0; bb < B; ++bb) if (off_rows[bb] == it.q_row0) b = bb;
       CHECK(b >= 0, "q_row0");
       const int M = it.n_cand * G;
-      const int want_kind = (M < (mfma_min_rows ? mfma_min_rows : 1) && M <= 4) ? 0 : (M + 15) / 16;
+      // mfma_min_rows 0 is the library's default, 3 (ss_round_desc)
+      const int want_kind = (M < (mfma_min_rows ? mfma_min_rows : 3) && M <= 4) ? 0 : (M + 15) / 16;
       CHECK(kind == want_kind, "unit kind %d want %d (M=%d)", kind, want_kind, M);
       int ntiles = 0;
       long toks = 0;
@@ -382,6 +383,10 @@ int main() {
     scenario("config2 per-chunk (no tail: small shares)", 1, 32, 8, {5}, {16384}, 2048, 0, layout, 8, 0, 0, 0);
     scenario("config5 batched 16", 32, 32, 8, std::vector<int>(32, 8), std::vector<int>(32, 131072), 8192, 0, layout, 16);
     scenario("many units (8192 chains)", 256, 8, 2, std::vector<int>(256, 3), std::vector<int>(256, 4096), 512, 128, layout, 8);
+    // one share of 2.2M tokens: with 8 KV heads token-major, a KV head's
+    // rows span more than 2^31 bytes, so the share is cut into pieces below
+    // that (32-bit buffer offsets)
+    scenario("one share over 2^31 bytes per head", 1, 8, 8, {2}, {2200000}, 2200000, 2199968, layout, 1);
     scenario("many items (chains of 16)", 128, 8, 2, std::vector<int>(128, 2), std::vector<int>(128, 8192), 32, 512, layout, 32);
     for (int rep = 0; rep < 40; ++rep) {
       const int B = 1 + rng() % 64;
@@ -392,8 +397,9 @@ int main() {
       int nch = 0; for (int x : h) nch = std::max(nch, (x + S - 1) / S);
       if (nch == 0) continue;
       const int batch = 1 + rng() % 32;
-      const int hsel = rng() % 4;   // GQA groups of 4, 4, 8 and 6 query heads
-      const int hq = hsel == 0 ? 32 : hsel == 1 ? 8 : hsel == 2 ? 64 : 48, hkv = hsel == 1 ? 2 : 8;
+      const int hsel = rng() % 6;   // GQA groups of 4, 4, 8, 6, 1 and 2 query heads
+      const int hq = hsel == 0 ? 32 : hsel == 1 ? 8 : hsel == 2 ? 64 : hsel == 3 ? 48 : hsel == 4 ? 8 : 16;
+      const int hkv = hsel == 1 ? 2 : 8;
       char nm[64]; snprintf(nm, sizeof nm, "random %d B=%d S=%d split=%d batch=%d", rep, B, S, split, batch);
       const int bal = (rng() % 4 == 0) ? -1 : (rng() % 2 ? 0 : (int)(1 + rng() % 500));
       scenario(nm, B, hq, hkv, nc, h, S, split, layout, batch, (int)(rng() % 6), bal);
