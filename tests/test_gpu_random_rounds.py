@@ -169,3 +169,48 @@ def test_table_capacities(stream, name):
     ref_o, ref_l = oracle_full(w)
     assert_parity(b.out.double().cpu().numpy(), ref_o, f"capacity {name}")
     assert_parity(b.lse.double().cpu().numpy(), ref_l, f"capacity {name} lse", max_abs=1e-3, rel_l2=1e-4)
+
+
+STREAMED_CASES = [k for k in range(NUM_CASES) if k % 3 == 0]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("k", STREAMED_CASES)
+def test_random_streamed_round(stream, k):
+    """The same random rounds with the history streamed from pinned host
+    memory through the two-slot pipeline: one chunk per transfer (in the
+    drawn order) or transfer batches of adjacent chunks.  The result equals,
+    bitwise, the in-HBM round that makes the same history calls, and
+    matches the oracle."""
+    c = draw_case(k)
+    w = W.custom(c["lens"], c["cands"], num_q_heads=c["hq"], num_kv_heads=c["hkv"],
+                 chunk_tokens=c["chunk_tokens"], seed_base=c["seed"], kscale=c["kscale"],
+                 outlier_per_10000=c["outliers"])
+    nch = w.num_chunks
+    if nch == 0:
+        pytest.skip("no history to stream")
+    batch = (1, 2, min(32, nch))[c["batch_choice"]]
+    order = list(np.random.default_rng(c["seed"]).permutation(nch)) if batch == 1 and c["shuffle"] else None
+    print(f"random streamed case {k}: chunks={nch} batch={batch} order={order} layout={c['layout']}", flush=True)
+    kw = dict(split_tokens=c["split"], mfma_min_rows=c["mfma_min_rows"], kv_layout=c["layout"],
+              balance_permille=c["balance"])
+    ref = H.RoundBuffers(w, **kw)
+    chunks = H.hbm_history(w, kv_layout=c["layout"])
+    torch.cuda.synchronize()
+    H.run_round(ref, chunks, stream.cuda_stream, order=order, batch=batch)
+    stream.synchronize()
+    del chunks
+    host = H.HostHistory(w, kv_layout=c["layout"])
+    pipe = H.Pipeline(H.batch_bytes(host, batch) if batch > 1 else host.max_chunk_bytes())
+    try:
+        b = H.RoundBuffers(w, **kw)
+        b.out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        H.run_round_streamed(b, host, pipe, stream.cuda_stream, order=order, batch=batch)
+        stream.synchronize()
+    finally:
+        pipe.close()
+    assert torch.equal(b.out, ref.out) and torch.equal(b.lse, ref.lse), f"streamed case {k} differs from in-HBM"
+    ref_o, ref_l = oracle_full(w)
+    assert_parity(b.out.double().cpu().numpy(), ref_o, f"streamed {k}")
+    assert_parity(b.lse.double().cpu().numpy(), ref_l, f"streamed {k} lse", max_abs=1e-3, rel_l2=1e-4)
