@@ -1085,7 +1085,7 @@ __global__ void __launch_bounds__(64) clear_counters_kernel(uint32_t *c, int n) 
 //   * merge the split slots the history calls wrote (Eq. 14; slot count per
 //     request from the host, unwritten slots are never read),
 //   * write O = a / l and LSE = m ln 2 + ln l (Eq. 17).
-// One wave per row (grid.y covers a request's rows, 4 per workgroup); lane l
+// One wave per row (4 rows of one request per workgroup); lane l
 // holds d = 2l, 2l+1.  The kernel is latency-bound, so a row costs one
 // memory round trip: every load is issued before any use (the query, the
 // visible candidates' K/V, each slot's m and l - lane s loads slot s - and
@@ -1095,12 +1095,19 @@ __global__ void __launch_bounds__(64) clear_counters_kernel(uint32_t *c, int n) 
 // rescaling.  Slot loads past the request's count go through empty buffer
 // resources or offsets past the end and read zeros.
 // ---------------------------------------------------------------------------
-template <int MS, typename P>
+//
+// The grid is (request, block of 4 rows), sized for the request with the
+// most rows; a block past a request's rows exits at once.  Workgroups are
+// dispatched in grid order, so with the requests as the fast dimension the
+// blocks of the requests with the most rows come last, behind every idle
+// block: with ragged row counts the grid is built the other way round
+// (RowsFast), which spreads the idle blocks over the dispatch.
+template <int MS, bool RowsFast, typename P>
 __global__ void __launch_bounds__(256) finalize_kernel(const P p) {
   const int w = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const Item it = p.items[blockIdx.x];
-  const int r = blockIdx.y * kWaves + w;          // local row = i * Hq + h
+  const Item it = p.items[RowsFast ? blockIdx.y : blockIdx.x];
+  const int r = (RowsFast ? blockIdx.x : blockIdx.y) * kWaves + w;   // local row = i * Hq + h
   if (r >= it.n_cand * p.Hq) return;
   const int i = r / p.Hq;
   const int h = r - i * p.Hq;
@@ -1276,17 +1283,23 @@ hipError_t launch_clear_counters(uint32_t *counters, int n, hipStream_t s) {
   hipLaunchKernelGGL(clear_counters_kernel, dim3(1), dim3(64), 0, s, counters, n);
   return hipGetLastError();
 }
-template <int MS>
-hipError_t launch_finalize_as(const FinalParams &p, dim3 grid, hipStream_t s) {
+template <int MS, bool RowsFast>
+hipError_t launch_finalize_as(const FinalParams &p, int row_blocks, hipStream_t s) {
+  const dim3 grid = RowsFast ? dim3(row_blocks, p.num_items) : dim3(p.num_items, row_blocks);
   if (p.num_items <= FinalSmall::kItems) {
     static thread_local FinalSmall d;
     static_cast<FinalHeader &>(d) = p;
     std::memcpy(d.items, p.items, sizeof(Item) * p.num_items);
-    hipLaunchKernelGGL((finalize_kernel<MS, FinalSmall>), grid, dim3(256), 0, s, d);
+    hipLaunchKernelGGL((finalize_kernel<MS, RowsFast, FinalSmall>), grid, dim3(256), 0, s, d);
   } else {
-    hipLaunchKernelGGL((finalize_kernel<MS, FinalParams>), grid, dim3(256), 0, s, p);
+    hipLaunchKernelGGL((finalize_kernel<MS, RowsFast, FinalParams>), grid, dim3(256), 0, s, p);
   }
   return hipGetLastError();
+}
+
+template <int MS>
+hipError_t launch_finalize_ms(const FinalParams &p, int row_blocks, bool rows_fast, hipStream_t s) {
+  return rows_fast ? launch_finalize_as<MS, true>(p, row_blocks, s) : launch_finalize_as<MS, false>(p, row_blocks, s);
 }
 
 hipError_t launch_finalize(const FinalParams &p, hipStream_t s) {
@@ -1295,16 +1308,27 @@ hipError_t launch_finalize(const FinalParams &p, hipStream_t s) {
   // request's slot count keeps more waves resident.  Measured on MI355X:
   // 16 x 32768 tokens (14 slots) 7.3 -> 6.0 us, 64 ragged requests (16
   // slots) 19.8 -> 13.6 us against the 32-slot build.
+  // Row-block order: the requests-fast grid keeps a request's blocks on one
+  // XCD (the grid's request count is a multiple of 8 in the common case),
+  // which measured faster for uniform cohorts; with more than a quarter of
+  // the blocks idle the rows-fast grid is faster.  Measured on MI355X
+  // (medians, alternated in one run): 64 ragged requests (42% idle) 16.5 us
+  // requests-fast, 14.5-14.9 us rows-fast; 16 x 6 candidates 6.8-7.0 us
+  // requests-fast, 7.0-7.1 us rows-fast.
   int rows = 0, slots = 0;
+  long busy = 0;
   for (int i = 0; i < p.num_items; ++i) {
-    rows = rows > p.items[i].n_cand * p.Hq ? rows : p.items[i].n_cand * p.Hq;
+    const int ri = p.items[i].n_cand * p.Hq;
+    rows = rows > ri ? rows : ri;
+    busy += (ri + kWaves - 1) / kWaves;
     slots = slots > p.items[i].tok_count ? slots : p.items[i].tok_count;
   }
-  const dim3 grid(p.num_items, (rows + kWaves - 1) / kWaves);
-  if (slots <= 8) return launch_finalize_as<8>(p, grid, s);
-  if (slots <= 16) return launch_finalize_as<16>(p, grid, s);
-  if (slots <= 24) return launch_finalize_as<24>(p, grid, s);
-  return launch_finalize_as<kNumSlots>(p, grid, s);
+  const int row_blocks = (rows + kWaves - 1) / kWaves;
+  const bool rows_fast = 4 * busy < 3 * (long)row_blocks * p.num_items;
+  if (slots <= 8) return launch_finalize_ms<8>(p, row_blocks, rows_fast, s);
+  if (slots <= 16) return launch_finalize_ms<16>(p, row_blocks, rows_fast, s);
+  if (slots <= 24) return launch_finalize_ms<24>(p, row_blocks, rows_fast, s);
+  return launch_finalize_ms<kNumSlots>(p, row_blocks, rows_fast, s);
 }
 
 hipError_t launch_read_probe(const void *buf, uint64_t bytes, uint64_t share, uint32_t *sink, int workgroups,
