@@ -295,7 +295,7 @@ __device__ __forceinline__ s16x4_t lds_read_tr16(const unsigned char *p) {
 }
 
 template <int RB, typename P>
-__device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, const UnitRec &ur, int tx, int g) {
+__device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, const UnitRec &ur, int tx, int g, int nxt) {
   const int w = __builtin_amdgcn_readfirstlane(tx >> 6);   // wave-uniform
   const int lane = tx & 63;
   const int lr = lane & 15;
@@ -475,6 +475,18 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, const
   // later item of the chain rebuilds its resources from that item.
   const FirstItem fi = load_first_item(p, ur);
   const Item &it = fi.it;
+  // The workgroup's next unit of its own list (nxt >= 0): its first item's
+  // resources, read now, so that each wave can bring the lines of its first
+  // tile of that unit into the L2 cache during its last tile of this one.
+  __amdgpu_buffer_rsrc_t wkrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.q), (short)0, 0, kBufferFlags);
+  __amdgpu_buffer_rsrc_t wvrs = wkrs;
+  if (nxt >= 0) {
+    const UnitRec un = p.units[nxt];
+    const Item in0 = p.items[unit_i0(un.word)];
+    const int cn = unit_chunk(un.word);
+    wkrs = item_rsrc(p, in0, cn, g, p.k);
+    wvrs = item_rsrc(p, in0, cn, g, p.v);
+  }
   int T = w;
   TileCursor cur;
   NextTile nx;
@@ -515,7 +527,19 @@ __device__ __forceinline__ void mfma_unit(const P &p, unsigned char *smem, const
       tb = nx.tb;
       count = p.items[i0 + cur.k].tok_count;
     }
+    // one 4-byte read per 128-byte line of this wave's first tile of the
+    // next unit (tokens 32w .. 32w+31 of its first item, K and V; reads
+    // past the item return zero without touching memory), at the default
+    // cache policy so the lines stay in L2; the values are only kept alive
+    // until the last tile is done, where the wait for them is free
+    uint32_t warm_k = 0, warm_v = 0;
+    if (nxt >= 0) {
+      const uint32_t wo = (uint32_t)(kTile * w + (lane >> 1)) * stride_b + 128u * (uint32_t)(lane & 1);
+      warm_k = __builtin_amdgcn_raw_buffer_load_b32(wkrs, wo, 0, 0);
+      warm_v = __builtin_amdgcn_raw_buffer_load_b32(wvrs, wo, 0, 0);
+    }
     tile(tb, count, std::integral_constant<bool, false>{}, nx);
+    asm volatile("" ::"v"(warm_k), "v"(warm_v));
   }
 
   // wave partials -> LDS
@@ -1055,10 +1079,11 @@ __global__ void __launch_bounds__(256, 2) chunk_attn(const P p) {
         continue;
       }
     }
+    const int nxt = u < more1 ? (int)u : -1;   // the next unit of the workgroup's own list
     if (kind == kUnitMfma2)
-      mfma_unit<2>(p, smem, ur, tx, g);
+      mfma_unit<2>(p, smem, ur, tx, g, nxt);
     else if (kind == kUnitMfma1)
-      mfma_unit<1>(p, smem, ur, tx, g);
+      mfma_unit<1>(p, smem, ur, tx, g, nxt);
     else {
       // the VALU body's work grows with the rows it is built for: build it
       // for 1, 2 and 4 rows and take the smallest that holds the unit
